@@ -1,0 +1,313 @@
+/*
+ * lmgc.h -- C ABI of liblmgc, an MI355X (gfx950) implementation of the LM-GC
+ * hot path: "Language Models as Zero-shot Lossless Gradient Compressors"
+ * (arXiv 2409.17836).
+ *
+ * The method (Sec. 3): serialise float32 gradients as hexadecimal text with a
+ * separator after every 4 bytes, run a causal language model over the token
+ * stream to get p(t_k | BOS, t_<k) for every token (Eq. 2), and use these
+ * probabilities as the model of an arithmetic coder (Sec. 2, "Arithmetic
+ * coding"); decompression replays the model from BOS token by token.
+ *
+ * Conventions
+ *   - Every call returns an int status (LMGC_OK or a negative LMGC_E* code)
+ *     unless stated otherwise; lmgc_last_error() gives a thread-local message.
+ *     No C++ exception or abort crosses this ABI.
+ *   - The caller owns every buffer.  "d_" pointers are device (HBM) pointers,
+ *     "h_"/plain pointers are host pointers.  Size helpers say how much to
+ *     allocate.
+ *   - GPU calls are asynchronous on the caller's stream (a hipStream_t passed
+ *     as void*; NULL = the default stream).  Host calls are synchronous.
+ *   - Layouts are row-major, little-endian.
+ *   - A model handle is immutable after lmgc_model_create and may be used
+ *     from several host threads with different workspaces.
+ */
+#ifndef LMGC_H
+#define LMGC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ----------------------------------------------------------------- status */
+#define LMGC_OK 0
+#define LMGC_EINVAL -1        /* bad argument or unsupported shape          */
+#define LMGC_ENOMEM -2        /* device or host allocation failed           */
+#define LMGC_EDEVICE -3       /* a HIP runtime call failed                  */
+#define LMGC_ESIZE -4         /* caller buffer too small                    */
+#define LMGC_ECORRUPT -5      /* malformed token stream, bitstream or container */
+#define LMGC_EUNSUPPORTED -6  /* valid request this build does not support  */
+
+/* Thread-local description of the last error on this thread ("" if none). */
+const char* lmgc_last_error(void);
+
+/* Library version string. */
+const char* lmgc_version(void);
+
+/* ---------------------------------------------------------- serialisation */
+/*
+ * Serialisation parameters (Sec. 3, "Serialization"; byte-grouping ablation
+ * in Sec. 4.3).  The value vector is read as a stream of bytes, each value's
+ * bytes most-significant first when msb_first=1 (sign/exponent digits lead,
+ * like printf("%08x")) or in memory (little-endian) order when msb_first=0;
+ * each byte gives two hex-digit tokens, high nibble first; a separator token
+ * follows every bytes_per_group bytes and the last (possibly partial) group.
+ * bytes_per_group = 0 means no separator (the paper's H_n).  With
+ * bytes_per_value = bytes_per_group = 4 every float32 is 8 digits + 1
+ * separator = 9 tokens.
+ *
+ * The stream is cut into consecutive windows of `window` tokens (the last
+ * one shorter; its tail is filled with pad_id).  The model input of a window
+ * is BOS followed by the window's tokens shifted by one, so position j is
+ * predicted from BOS and tokens 0..j-1 (Eq. 2); BOS is never coded.
+ *
+ * Coder bins: 0..15 = hex digit value, 16 = separator, 17 = escape (the rest
+ * of the vocabulary; never coded).  Token ids of bins 0..16 are hex_ids[] and
+ * sep_id; all ids must be < the model's vocabulary.
+ */
+typedef struct {
+  int32_t bytes_per_value; /* 4 (float32) | 2 | 1 (8-bit indices) */
+  int32_t bytes_per_group; /* >= 0 */
+  int32_t msb_first;       /* 1 or 0 */
+  int32_t window;          /* W > 0 */
+  int32_t bos_id;
+  int32_t pad_id;
+  int32_t sep_id;
+  int32_t hex_ids[16];
+} lmgc_serial_params;
+
+#define LMGC_NALPHA 17 /* coded alphabet: 16 digits + separator   */
+#define LMGC_NSYM 18   /* coder bins: alphabet + escape            */
+
+/* Tokens in the serialised stream of n_values values (>= 0), or < 0 on error. */
+int64_t lmgc_num_tokens(int64_t n_values, const lmgc_serial_params* p);
+/* Windows the stream is cut into (ceil(tokens / W)), or < 0 on error. */
+int64_t lmgc_num_windows(int64_t n_values, const lmgc_serial_params* p);
+
+/*
+ * Serialise windows [first_window, first_window + n_windows) of the stream of
+ * d_values (n_values values of bytes_per_value bytes, device memory).
+ *   d_tokens: [n_windows, W] int32 token ids; positions past the end of the
+ *             stream get pad_id.
+ *   d_sym:    nullable; [n_windows, W] uint8 coder bins (255 past the end).
+ * GPU, async on stream.  Errors: EINVAL (bad params or window range).
+ */
+int lmgc_serialize(const void* d_values, int64_t n_values, const lmgc_serial_params* p,
+                   int64_t first_window, int64_t n_windows, int32_t* d_tokens,
+                   uint8_t* d_sym, void* stream);
+
+/*
+ * Host inverse on coder bins: sym[n_tokens] -> values_out (n_values *
+ * bytes_per_value bytes).  ECORRUPT if a digit or separator is out of place,
+ * a bin is out of range or n_tokens does not match n_values.
+ */
+int lmgc_deserialize(const uint8_t* sym, int64_t n_tokens, int64_t n_values,
+                     const lmgc_serial_params* p, void* values_out);
+
+/* ------------------------------------------------------------------ model */
+enum { LMGC_ARCH_LLAMA = 0, LMGC_ARCH_GPT2 = 1 };
+enum { LMGC_DTYPE_F32 = 0, LMGC_DTYPE_BF16 = 1 };
+
+/*
+ * Decoder shape.  LLAMA: RMSNorm, RoPE (rotate-half, theta), SwiGLU FFN,
+ * grouped-query attention (kv head of query head h = h*n_kv_heads/n_heads),
+ * untied LM head.  GPT2: LayerNorm with bias, learned positions (max_pos),
+ * biased projections, tanh-GELU FFN, head tied to the token embedding.
+ * Requirements: d_model = n_heads * head_dim; head_dim in {64, 128} for BF16
+ * and 16..64 (multiple of 16) for F32; d_model and d_ff multiples of 64.
+ */
+typedef struct {
+  int32_t arch;       /* LMGC_ARCH_* */
+  int32_t dtype;      /* LMGC_DTYPE_*: parameters and matrix-product operands */
+  int32_t n_layers;
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t n_kv_heads;
+  int32_t d_ff;
+  int32_t vocab;
+  int32_t max_pos;    /* longest window the model accepts */
+  float rope_theta;
+  float norm_eps;
+} lmgc_model_config;
+
+typedef struct lmgc_model lmgc_model;
+
+/* Number of parameter tensors of a config, or < 0 on error. */
+int32_t lmgc_model_num_tensors(const lmgc_model_config* cfg);
+
+/*
+ * Name (NUL-terminated, truncated to name_cap) and shape of manifest tensor
+ * `index`.  Matrices are [out, in]: row n holds the weights of output
+ * feature n.  LLAMA order: tok_emb[V,d]; per layer l: l{l}.attn_norm[d],
+ * wq[Hq*hd,d], wk[Hkv*hd,d], wv[Hkv*hd,d], wo[d,Hq*hd], ffn_norm[d],
+ * w_gate[F,d], w_up[F,d], w_down[d,F]; final_norm[d], lm_head[V,d].
+ * GPT2 order: wte[V,d], wpe[max_pos,d]; per layer: ln1_g, ln1_b, w_qkv[3d,d],
+ * b_qkv[3d], w_o[d,d], b_o[d], ln2_g, ln2_b, w_fc[F,d], b_fc[F],
+ * w_proj[d,F], b_proj[d]; lnf_g[d], lnf_b[d].
+ */
+int lmgc_model_tensor_info(const lmgc_model_config* cfg, int32_t index, char* name,
+                           size_t name_cap, int32_t* ndim, int64_t shape[2]);
+
+/*
+ * Create a model from device tensors in manifest order, each of the config's
+ * dtype (bfloat16 bit patterns for BF16).  The handle copies and repacks
+ * what it needs into its own device memory (the caller may free the inputs
+ * after the call returns).  Synchronises `stream`.
+ * Errors: EINVAL (bad config), ENOMEM, EDEVICE.
+ */
+int lmgc_model_create(const lmgc_model_config* cfg, const void* const* d_weights,
+                      void* stream, lmgc_model** out);
+void lmgc_model_destroy(lmgc_model* m);
+
+/* Bytes of device workspace lmgc_probs needs for B windows of W tokens. */
+size_t lmgc_probs_workspace(const lmgc_model* m, int32_t B, int32_t W);
+
+/*
+ * The LM as the coder's model (Sec. 3, "Compression": P_AC = P_LM).
+ * d_tokens: [B, W] int32 data tokens of B windows (the BOS shift is done
+ * here).  For every window b and position j < W:
+ *   lp[a]  = log p(alphabet token a | BOS, tokens[b, 0..j-1]), normalised
+ *            over the whole vocabulary (float32, a = 0..16);
+ *   f[a]   = 1 + floor(exp(lp[a]) * (total - 18)) (in double), the largest
+ *            giving up any excess over total-1 (lowest index on ties);
+ *   f[17]  = total - sum(f[0..16])  (escape bin, never coded);
+ *   d_cdf[b, j, 0..18] = 0, f0, f0+f1, ..., total.
+ * d_logp (nullable) receives lp as [B, W, 17] float32.
+ * Row (b, j) is a bitwise function of the weights and tokens[b, 0..j-1]
+ * only: it does not depend on later tokens, on other windows, on B or on W.
+ * total must be in [18*2, 2^24].  GPU, async.  Errors: EINVAL, ESIZE (ws).
+ */
+int lmgc_probs(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t W,
+               const lmgc_serial_params* p, uint32_t total, uint32_t* d_cdf, float* d_logp,
+               void* d_ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------- coding */
+/*
+ * Arithmetic coding (Sec. 2): a Witten-Neal-Cleary binary arithmetic coder
+ * with 62-bit code values.  Each window is an independent bitstream, packed
+ * most significant bit first and padded with zero bits to a whole byte.
+ * Flush: pending+1 bits, the first 0 if low < 1/4 else 1.
+ */
+/* Upper bound of the payload bytes lmgc_encode writes for these windows. */
+size_t lmgc_encode_bound(int32_t n_win, int32_t W);
+
+/*
+ * Host.  cdf: [n_win, W, nsym+1] uint32 tables (cdf[..., nsym] = total);
+ * sym: [n_win, W] bins; len[w] <= W symbols of window w are coded.
+ * Writes the windows' payloads back to back into out (cap bytes); bits[w]
+ * gets window w's exact bit count and *used the bytes written.
+ * n_threads <= 0 picks a default.  Errors: EINVAL, ESIZE, ECORRUPT (a symbol
+ * with zero frequency or out of range).
+ */
+int lmgc_encode(const uint32_t* cdf, int32_t nsym, const uint8_t* sym, const int32_t* len,
+                int32_t n_win, int32_t W, uint8_t* out, size_t cap, uint32_t* bits,
+                size_t* used, int32_t n_threads);
+
+/* Symbol-at-a-time decoder state (opaque). */
+typedef struct {
+  uint64_t opaque[8];
+} lmgc_decoder;
+
+int lmgc_decode_init(lmgc_decoder* st, const uint8_t* payload, uint64_t nbits);
+/* Decode one symbol with model row cdf_row[nsym+1]; *sym_out gets the bin. */
+int lmgc_decode_symbol(lmgc_decoder* st, const uint32_t* cdf_row, int32_t nsym,
+                       int32_t* sym_out);
+
+/* -------------------------------------------------------------- container */
+/*
+ * Container (little-endian): 128-byte header
+ *   0 "LMGC" | 4 u16 version=1 | 6 u16 header bytes=128 | 8 u64 model tag |
+ *   16 u64 n_values | 24 u8 bytes_per_value | 25 u8 bytes_per_group |
+ *   26 u8 msb_first | 27 u8 nsym=18 | 28 u32 W | 32 u32 total |
+ *   36 u32 n_windows | 40 i32 bos | 44 i32 pad | 48 i32 sep | 52 i32 hex[16] |
+ *   116..127 zero
+ * then u32 bits[n_windows], then the payloads, each ceil(bits/8) bytes.
+ */
+#define LMGC_HEADER_BYTES 128
+
+/* Upper bound of the container size for n_values values. */
+size_t lmgc_container_bound(int64_t n_values, const lmgc_serial_params* p);
+
+/* Device workspace bytes lmgc_compress / lmgc_decode need. */
+size_t lmgc_codec_workspace(const lmgc_model* m, int64_t n_values, const lmgc_serial_params* p,
+                            int32_t batch);
+
+/*
+ * Compress d_values (device) into a container at out (host).  Windows
+ * [first_window, first_window + n_windows) are coded (n_windows < 0: all
+ * windows from first_window on); the header records all of the vector's
+ * windows only when the whole vector is coded.  batch windows per LM call;
+ * host coding of one batch overlaps the GPU work of the next.  Synchronises
+ * stream before returning.  Errors: EINVAL, ESIZE (cap or ws), EDEVICE.
+ */
+int lmgc_compress(const lmgc_model* m, const void* d_values, int64_t n_values,
+                  const lmgc_serial_params* p, uint32_t total, int32_t batch,
+                  uint64_t model_tag, int64_t first_window, int64_t n_windows,
+                  void* d_ws, size_t ws_bytes, uint8_t* out, size_t cap, size_t* used,
+                  void* stream);
+
+/*
+ * Decompress a whole-vector container into values_out (host, n_values *
+ * bytes_per_value bytes).  Decodes window batches token by token from BOS,
+ * re-running lmgc_probs on the decoded prefix at every step.  expect_tag
+ * must equal the header's model tag.  Errors: ECORRUPT (bad container,
+ * escape symbol, malformed stream, tag mismatch), ESIZE, EDEVICE.
+ */
+int lmgc_decode(const lmgc_model* m, const uint8_t* container, size_t bytes, int32_t batch,
+                uint64_t expect_tag, void* d_ws, size_t ws_bytes, void* values_out,
+                void* stream);
+
+/* Parse a container header: n_values and windows, for sizing buffers. */
+int lmgc_container_info(const uint8_t* container, size_t bytes, int64_t* n_values,
+                        int32_t* bytes_per_value, int64_t* n_windows, uint64_t* model_tag);
+
+/* ----------------------------------------------------- kernel-level calls */
+/*
+ * C[M, N] (float32) = A[M, K] * B[N, K]^T with bfloat16 A, B (bit patterns)
+ * and float32 accumulation: the matrix-product kernel of the decoder's
+ * projections (Sec. 4.1 LLMs), exposed for parity tests at full size.
+ * K must be a multiple of 64.  GPU, async.
+ */
+int lmgc_op_gemm_bf16(const uint16_t* d_a, const uint16_t* d_b, float* d_c, int32_t M,
+                      int32_t N, int32_t K, void* stream);
+
+/*
+ * Causal attention kernel on bfloat16 operands: q [B, Hq, W, hd],
+ * k [B, Hkv, W, hd], vt [B, Hkv, hd, W] (v transposed) -> o [B*W, Hq*hd]
+ * bfloat16, softmax of q.k/sqrt(hd) over keys <= query.  hd in {64, 128}.
+ */
+int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_vt,
+                           uint16_t* d_o, int32_t B, int32_t Hq, int32_t Hkv, int32_t W,
+                           int32_t hd, void* stream);
+
+/* ------------------------------------------------------------------ timing */
+/*
+ * Per-kernel timing with HIP events recorded around each launch lmgc_probs
+ * makes on its stream.  Kinds index the dominant kernels.
+ */
+enum {
+  LMGC_K_EMBED = 0,
+  LMGC_K_NORM = 1,
+  LMGC_K_GEMM_QKV = 2,
+  LMGC_K_ATTN = 3,
+  LMGC_K_GEMM_O = 4,
+  LMGC_K_GEMM_UP = 5,   /* gate/up with SwiGLU (LLAMA) or fc with GELU (GPT2) */
+  LMGC_K_GEMM_DOWN = 6,
+  LMGC_K_GEMM_HEAD = 7,
+  LMGC_K_LSE_CDF = 8,
+  LMGC_K_COUNT = 9
+};
+/* Enable (1) or disable (0) timing and clear the accumulated times. */
+int lmgc_timing_enable(int32_t enable);
+/* Synchronise pending events; total milliseconds and launches of `kind`. */
+int lmgc_timing_read(int32_t kind, double* total_ms, int64_t* count);
+/* Algorithmic floating-point operations of one lmgc_probs call, by kind. */
+double lmgc_probs_flops(const lmgc_model* m, int32_t B, int32_t W, int32_t kind);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LMGC_H */

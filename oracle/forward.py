@@ -44,12 +44,29 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     return np.ldexp(np.rint(m * 256.0) / 256.0, e)
 
 
-def storage_to_f64(w: np.ndarray, dtype: str) -> np.ndarray:
-    """Decode stored parameters: bf16 bit patterns (uint16) or float32."""
+def _decode_chunk(w: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         assert w.dtype == np.uint16
         return (w.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
     return np.asarray(w, dtype=np.float32).astype(np.float64)
+
+
+def storage_to_f64(w: np.ndarray, dtype: str) -> np.ndarray:
+    """Decode stored parameters: bf16 bit patterns (uint16) or float32.
+    Large tensors are decoded in row chunks on several threads."""
+    if w.size < (1 << 22) or w.ndim < 2:
+        return _decode_chunk(w, dtype)
+    from concurrent.futures import ThreadPoolExecutor
+    import os
+    out = np.empty(w.shape, np.float64)
+    step = max(1, w.shape[0] // 32)
+
+    def run(r0):
+        out[r0:r0 + step] = _decode_chunk(w[r0:r0 + step], dtype)
+
+    with ThreadPoolExecutor(max(1, min(16, os.cpu_count() or 1))) as ex:
+        list(ex.map(run, range(0, w.shape[0], step)))
+    return out
 
 
 def rms_norm(h, g, eps):
@@ -125,24 +142,31 @@ class Model:
 
     # -- one sequence, all positions --------------------------------------
     def final_hidden(self, x: np.ndarray) -> np.ndarray:
-        """x: [n] model input ids (BOS first) -> bf16-rounded normed final
-        state [n, d] that feeds the LM head."""
+        """x: [n] (or [nb, n] independent windows) model input ids, BOS
+        first -> bf16-rounded normed final state [..., n, d] that feeds the
+        LM head."""
         m, rnd, w = self.m, self.rnd, self.w
-        n = x.shape[0]
+        n = x.shape[-1]
+        lead = x.shape[:-1]
         hd = m.head_dim
         pos = np.arange(n)
+
+        def attend(q, k, v):
+            if not lead:
+                return causal_attention(q, k, v)
+            return np.stack([causal_attention(q[i], k[i], v[i]) for i in range(q.shape[0])])
         if m.arch == "llama":
             h = w("tok_emb")[x]
             for l in range(m.n_layers):
                 p = f"l{l}."
                 a = rnd(rms_norm(h, w(p + "attn_norm"), m.norm_eps))
-                q = (a @ w(p + "wq").T).reshape(n, m.n_heads, hd)
-                k = (a @ w(p + "wk").T).reshape(n, m.n_kv_heads, hd)
-                v = (a @ w(p + "wv").T).reshape(n, m.n_kv_heads, hd)
+                q = (a @ w(p + "wq").T).reshape(*lead, n, m.n_heads, hd)
+                k = (a @ w(p + "wk").T).reshape(*lead, n, m.n_kv_heads, hd)
+                v = (a @ w(p + "wv").T).reshape(*lead, n, m.n_kv_heads, hd)
                 q = rnd(rope(q, pos, m.rope_theta))
                 k = rnd(rope(k, pos, m.rope_theta))
                 v = rnd(v)
-                o = rnd(causal_attention(q, k, v))
+                o = rnd(attend(q, k, v))
                 h = h + o @ w(p + "wo").T
                 b = rnd(rms_norm(h, w(p + "ffn_norm"), m.norm_eps))
                 act = rnd(silu(b @ w(p + "w_gate").T) * (b @ w(p + "w_up").T))
@@ -155,10 +179,10 @@ class Model:
                 p = f"l{l}."
                 a = rnd(layer_norm(h, w(p + "ln1_g"), w(p + "ln1_b"), m.norm_eps))
                 qkv = a @ w(p + "w_qkv").T + w(p + "b_qkv")
-                q = rnd(qkv[:, :d]).reshape(n, m.n_heads, hd)
-                k = rnd(qkv[:, d:2 * d]).reshape(n, m.n_heads, hd)
-                v = rnd(qkv[:, 2 * d:]).reshape(n, m.n_heads, hd)
-                o = rnd(causal_attention(q, k, v))
+                q = rnd(qkv[..., :d]).reshape(*lead, n, m.n_heads, hd)
+                k = rnd(qkv[..., d:2 * d]).reshape(*lead, n, m.n_heads, hd)
+                v = rnd(qkv[..., 2 * d:]).reshape(*lead, n, m.n_heads, hd)
+                o = rnd(attend(q, k, v))
                 h = h + (o @ w(p + "w_o").T + w(p + "b_o"))
                 c = rnd(layer_norm(h, w(p + "ln2_g"), w(p + "ln2_b"), m.norm_eps))
                 f = rnd(gelu_tanh(c @ w(p + "w_fc").T + w(p + "b_fc")))
@@ -170,12 +194,12 @@ class Model:
         return self.w("lm_head") if self.m.arch == "llama" else self.w("wte")
 
     def logits(self, x: np.ndarray) -> np.ndarray:
-        """x: [n] -> logits [n, V]."""
+        """x: [..., n] -> logits [..., n, V]."""
         return self.final_hidden(x) @ self.head_matrix().T
 
     def alphabet_logprobs(self, x: np.ndarray, ids) -> np.ndarray:
-        """x: [n] -> [n, len(ids)] natural-log probabilities of the given ids,
-        normalised over the whole vocabulary (Eq. 2)."""
+        """x: [..., n] -> [..., n, len(ids)] natural-log probabilities of the
+        given ids, normalised over the whole vocabulary (Eq. 2)."""
         return logprobs_from_logits(self.logits(x), ids)
 
 

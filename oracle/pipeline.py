@@ -105,8 +105,15 @@ def compress(values: np.ndarray, serial, model: Model, model_tag: int = 0,
     wins = windows(tok.size, serial.window)
     if incremental:
         lp_rows = _incremental_logprobs(model, tok, wins, serial)
+    elif wins:
+        # all windows in one batched pass; positions past a window's end hold
+        # pad tokens and, by causality, do not change the positions before it
+        nmax = max(n for _, n in wins)
+        X = np.stack([model_input(tok[s:s + n], serial, nmax) for s, n in wins])
+        lp = model.alphabet_logprobs(X, alphabet_ids(serial))
+        lp_rows = [lp[w, :n] for w, (_, n) in enumerate(wins)]
     else:
-        lp_rows = [window_logprobs(model, tok[s:s + n], serial) for s, n in wins]
+        lp_rows = []
     bits, payloads = [], []
     for (s, n), lp in zip(wins, lp_rows):
         cdf = coder.quantize(lp.astype(np.float32), total)

@@ -1,0 +1,98 @@
+// Internal declarations shared by the liblmgc translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/lmgc.h"
+
+namespace lmgc {
+
+// ------------------------------------------------------------ bf16 helpers
+__host__ __device__ inline float bf16_to_f32(uint16_t b) {
+  union { uint32_t u; float f; } v;
+  v.u = (uint32_t)b << 16;
+  return v.f;
+}
+
+// Round to nearest even; NaN stays NaN.
+__host__ __device__ inline uint16_t f32_to_bf16(float f) {
+  union { uint32_t u; float f; } v;
+  v.f = f;
+  uint32_t u = v.u;
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// ------------------------------------------------------- epilogue selectors
+// What the matrix-product kernels do with each output pair (col, col + 32).
+enum EpiKind : int {
+  EPI_STORE_F32 = 0,   // C[row, col] = v                          (float)
+  EPI_RESID = 1,       // h[row, col] += v (+ bias[col])            (float)
+  EPI_QKV_ROPE = 2,    // RoPE on q/k pairs, scatter to q, k, v      (act)
+  EPI_QKV_BIAS = 3,    // + bias, scatter to q, k, v (no RoPE)       (act)
+  EPI_SWIGLU = 4,      // out[row, f] = silu(gate) * up              (act)
+  EPI_BIAS_GELU = 5,   // out[row, col] = gelu_tanh(v + bias[col])   (act)
+};
+
+// Arguments of every epilogue (unused fields ignored).
+struct EpiArgs {
+  int kind;
+  int M, N;            // valid output extent (N = real columns)
+  // EPI_STORE_F32 / EPI_RESID
+  float* c;            // [M, ldc]
+  int ldc;
+  const void* bias;    // [N] model dtype, nullable
+  // attention layout scatter: q [B,Hq,W,hd], k [B,Hkv,W,hd],
+  // v [B,Hkv,hd,W] (bf16 models, transposed) or [B,Hkv,W,hd] (f32 models)
+  void* q;
+  void* k;
+  void* v;
+  int W, Hq, Hkv, hd;
+  const float2* rope;  // [max_pos, hd/2] (cos, sin)
+  // SWIGLU / GELU output
+  void* out;           // [M, ld_out]
+  int ld_out;
+};
+
+// ------------------------------------------------------------ launchers
+// All launchers return hipError_t of the launch.
+hipError_t launch_serialize(const void* values, int64_t n_values, const lmgc_serial_params& p,
+                            int64_t first_window, int64_t n_windows, int32_t* tokens,
+                            uint8_t* sym, hipStream_t s);
+
+// Token ids outside [0, vocab) are clamped (callers validate them).
+hipError_t launch_embed(const int32_t* tokens, int B, int W, int bos_id, const void* tok_emb,
+                        const void* pos_emb, int d, int vocab, int dtype, float* h, hipStream_t s);
+
+// y = norm(h) (rms if ln_bias == nullptr && !layernorm) in model dtype.
+hipError_t launch_norm(const float* h, int M, int d, const void* gain, const void* bias,
+                       int layernorm, float eps, int dtype, void* y, hipStream_t s);
+
+hipError_t launch_gemm_bf16(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
+                            const EpiArgs& e, hipStream_t s);
+hipError_t launch_gemm_f32(const float* A, const float* B, int M, int N_pad, int K,
+                           const EpiArgs& e, hipStream_t s);
+
+hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
+                                 uint16_t* o, int B, int Hq, int Hkv, int W, int hd,
+                                 hipStream_t s);
+hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,
+                                int B, int Hq, int Hkv, int W, int hd, hipStream_t s);
+
+// logits [M, ldz] (first V valid) -> cdf [M, 19], logp [M, 17] (nullable);
+// alpha_ids is a host array of the 17 alphabet token ids.
+hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
+                          uint32_t total, uint32_t* cdf, float* logp, hipStream_t s);
+
+// dst[r, :] = srcs.p[idx[r] >> 28][(idx[r] & 0x0fffffff), :] for r < rows;
+// idx[r] == -1 gives a zero row.  Rows are cols * elem_bytes bytes (multiple of 4).
+struct GatherSrcs {
+  const void* p[4];
+};
+hipError_t launch_gather_rows(GatherSrcs srcs, const int32_t* idx, int rows, int cols,
+                              int elem_bytes, void* dst, hipStream_t s);
+
+}  // namespace lmgc

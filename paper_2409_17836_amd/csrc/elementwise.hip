@@ -1,0 +1,238 @@
+// Row-wise kernels of the decoder: embedding with the BOS shift, RMSNorm /
+// LayerNorm, the log-sum-exp + integer-table kernel at the LM head, and the
+// row gather used to repack weights.  All are HBM-bound; each uses one
+// 64-wide wavefront per row with fixed-order (butterfly) reductions, so every
+// row's result is a bitwise function of that row alone.
+#include <math.h>
+
+#include "common.h"
+
+namespace lmgc {
+namespace {
+
+constexpr int kWave = 64;
+
+struct AlphaIds {
+  int32_t v[LMGC_NALPHA];
+};
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+__device__ inline float load_param(const void* p, int i, int dtype) {
+  return dtype == LMGC_DTYPE_BF16 ? bf16_to_f32(((const uint16_t*)p)[i]) : ((const float*)p)[i];
+}
+
+// ------------------------------------------------------------------ embed
+// h[b*W + j, :] = E[x] (+ P[j]) with x = BOS for j = 0, else tokens[b, j-1].
+__global__ void embed_kernel(const int32_t* __restrict__ tokens, int B, int W, int bos,
+                             const void* __restrict__ E, const void* __restrict__ P, int d,
+                             int V, int dtype, float* __restrict__ h) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (row >= (int64_t)B * W) return;
+  const int j = (int)(row % W);
+  const int x = min(max(j == 0 ? bos : tokens[row - 1], 0), V - 1);
+  float* out = h + row * d;
+  for (int c = lane * 4; c < d; c += kWave * 4) {
+    float4 v;
+    v.x = load_param(E, x * d + c + 0, dtype);
+    v.y = load_param(E, x * d + c + 1, dtype);
+    v.z = load_param(E, x * d + c + 2, dtype);
+    v.w = load_param(E, x * d + c + 3, dtype);
+    if (P) {
+      v.x += load_param(P, j * d + c + 0, dtype);
+      v.y += load_param(P, j * d + c + 1, dtype);
+      v.z += load_param(P, j * d + c + 2, dtype);
+      v.w += load_param(P, j * d + c + 3, dtype);
+    }
+    *reinterpret_cast<float4*>(out + c) = v;
+  }
+}
+
+// ------------------------------------------------------------------- norms
+// One wave per row; lane l keeps elements l, l+64, ... in registers.
+template <int MAXV>
+__global__ void norm_kernel(const float* __restrict__ h, int M, int d, const void* __restrict__ g,
+                            const void* __restrict__ b, int layernorm, float eps, int dtype,
+                            void* __restrict__ y) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (row >= M) return;
+  const float* x = h + row * d;
+  float v[MAXV];
+  const int nv = d / kWave;
+#pragma unroll
+  for (int i = 0; i < MAXV; i++)
+    if (i < nv) v[i] = x[i * kWave + lane];
+  float mean = 0.f;
+  if (layernorm) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < MAXV; i++)
+      if (i < nv) s += v[i];
+    mean = wave_sum(s) / (float)d;
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXV; i++) {
+    if (i < nv) {
+      const float a = v[i] - mean;
+      ss += a * a;
+    }
+  }
+  const float r = 1.0f / sqrtf(wave_sum(ss) / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < MAXV; i++) {
+    if (i >= nv) continue;
+    const int c = i * kWave + lane;
+    float t = (v[i] - mean) * r * load_param(g, c, dtype);
+    if (layernorm) t += load_param(b, c, dtype);
+    if (dtype == LMGC_DTYPE_BF16)
+      ((uint16_t*)y)[row * d + c] = f32_to_bf16(t);
+    else
+      ((float*)y)[row * d + c] = t;
+  }
+}
+
+// ------------------------------------------------------------ LSE + table
+// One wave per row: online max / sum-exp over the V logits, then the 17
+// alphabet log-probabilities and their integer table (quantised in double).
+__global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int V,
+                               AlphaIds ids, uint32_t total,
+                               uint32_t* __restrict__ cdf, float* __restrict__ logp) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (row >= M) return;
+  const float* zr = z + row * (int64_t)ldz;
+  float m = -INFINITY, s = 0.f;
+  const int V4 = V & ~3;
+  for (int c = lane * 4; c < V4; c += kWave * 4) {
+    const float4 t = *reinterpret_cast<const float4*>(zr + c);
+    const float mx = fmaxf(fmaxf(t.x, t.y), fmaxf(t.z, t.w));
+    const float mn = fmaxf(m, mx);
+    s = s * expf(m - mn) + ((expf(t.x - mn) + expf(t.y - mn)) + (expf(t.z - mn) + expf(t.w - mn)));
+    m = mn;
+  }
+  for (int c = V4 + lane; c < V; c += kWave) {
+    const float t = zr[c];
+    const float mn = fmaxf(m, t);
+    s = s * expf(m - mn) + expf(t - mn);
+    m = mn;
+  }
+  // merge (m, s) across the wave in a fixed butterfly
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float mo = __shfl_xor(m, o, kWave);
+    const float so = __shfl_xor(s, o, kWave);
+    const float mn = fmaxf(m, mo);
+    const float a = (m == -INFINITY) ? 0.f : s * expf(m - mn);
+    const float c = (mo == -INFINITY) ? 0.f : so * expf(mo - mn);
+    s = a + c;  // commutative: every lane gets the same bits
+    m = mn;
+  }
+  const float lse = m + logf(s);
+  uint32_t f = 0;
+  float lp = 0.f;
+  if (lane < LMGC_NALPHA) {
+    lp = zr[ids.v[lane]] - lse;
+    const double p = exp((double)lp);
+    f = 1u + (uint32_t)floor(p * (double)(total - LMGC_NSYM));
+    if (logp) logp[row * LMGC_NALPHA + lane] = lp;
+  }
+  uint32_t fa[LMGC_NALPHA];
+  uint64_t S = 0;
+#pragma unroll
+  for (int a = 0; a < LMGC_NALPHA; a++) {
+    fa[a] = (uint32_t)__shfl((int)f, a, kWave);
+    S += fa[a];
+  }
+  if (S > (uint64_t)(total - 1)) {
+    int big = 0;
+#pragma unroll
+    for (int a = 1; a < LMGC_NALPHA; a++)
+      if (fa[a] > fa[big]) big = a;
+    const uint32_t ex = (uint32_t)(S - (total - 1));
+#pragma unroll
+    for (int a = 0; a < LMGC_NALPHA; a++)
+      if (a == big) fa[a] -= ex;
+    S = total - 1;
+  }
+  if (lane <= LMGC_NSYM) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int a = 0; a < LMGC_NALPHA; a++)
+      if (a < lane) c += fa[a];
+    if (lane == LMGC_NSYM) c = total;
+    cdf[row * (LMGC_NSYM + 1) + lane] = c;
+  }
+}
+
+// ------------------------------------------------------------------ gather
+__global__ void gather_rows_kernel(GatherSrcs srcs, const int32_t* __restrict__ idx, int rows,
+                                   int words, uint32_t* __restrict__ dst) {
+  const int r = blockIdx.x;
+  if (r >= rows) return;
+  const int32_t id = idx[r];
+  uint32_t* out = dst + (int64_t)r * words;
+  if (id < 0) {
+    for (int c = threadIdx.x; c < words; c += blockDim.x) out[c] = 0u;
+    return;
+  }
+  const uint32_t* src = (const uint32_t*)srcs.p[id >> 28] + (int64_t)(id & 0x0fffffff) * words;
+  for (int c = threadIdx.x; c < words; c += blockDim.x) out[c] = src[c];
+}
+
+}  // namespace
+
+hipError_t launch_embed(const int32_t* tokens, int B, int W, int bos_id, const void* tok_emb,
+                        const void* pos_emb, int d, int vocab, int dtype, float* h, hipStream_t s) {
+  const int64_t rows = (int64_t)B * W;
+  hipLaunchKernelGGL(embed_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, tokens,
+                     B, W, bos_id, tok_emb, pos_emb, d, vocab, dtype, h);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm(const float* h, int M, int d, const void* gain, const void* bias,
+                       int layernorm, float eps, int dtype, void* y, hipStream_t s) {
+  const dim3 grid((unsigned)((M + 3) / 4));
+  if (d % kWave != 0 || d > 8192) return hipErrorInvalidValue;
+  if (d <= 1024)
+    hipLaunchKernelGGL(norm_kernel<16>, grid, dim3(256), 0, s, h, M, d, gain, bias, layernorm,
+                       eps, dtype, y);
+  else if (d <= 4096)
+    hipLaunchKernelGGL(norm_kernel<64>, grid, dim3(256), 0, s, h, M, d, gain, bias, layernorm,
+                       eps, dtype, y);
+  else
+    hipLaunchKernelGGL(norm_kernel<128>, grid, dim3(256), 0, s, h, M, d, gain, bias, layernorm,
+                       eps, dtype, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
+                          uint32_t total, uint32_t* cdf, float* logp, hipStream_t s) {
+  AlphaIds ids;
+  for (int a = 0; a < LMGC_NALPHA; a++) ids.v[a] = alpha_ids[a];
+  hipLaunchKernelGGL(lse_cdf_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, logits, M,
+                     ldz, V, ids, total, cdf, logp);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(GatherSrcs srcs, const int32_t* idx, int rows, int cols,
+                              int elem_bytes, void* dst, hipStream_t s) {
+  const int words = cols * elem_bytes / 4;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)rows), dim3(256), 0, s, srcs, idx, rows,
+                     words, (uint32_t*)dst);
+  return hipGetLastError();
+}
+
+}  // namespace lmgc

@@ -24,8 +24,12 @@ def _threads() -> int:
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float32 to the nearest bfloat16 (ties to even); returns uint16 bits."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
-    return r.astype(np.uint16)
+    t = u >> np.uint32(16)
+    t &= np.uint32(1)
+    t += np.uint32(0x7FFF)
+    t += u
+    t >>= np.uint32(16)
+    return t.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -137,7 +141,8 @@ def _role(name: str) -> str:
     return "matrix"
 
 
-def _normal_f32(shape, seed: int, idx: int, pool: ThreadPoolExecutor) -> np.ndarray:
+def _normal_f32(shape, seed: int, idx: int, pool: ThreadPoolExecutor,
+                scale: float = 1.0) -> np.ndarray:
     n = int(np.prod(shape))
     out = np.empty(n, np.float32)
     ss = np.random.SeedSequence(entropy=seed, spawn_key=(idx,))
@@ -147,6 +152,8 @@ def _normal_f32(shape, seed: int, idx: int, pool: ThreadPoolExecutor) -> np.ndar
         lo = c * _CHUNK
         hi = min(n, lo + _CHUNK)
         np.random.default_rng(kids[c]).standard_normal(out=out[lo:hi], dtype=np.float32)
+        if scale != 1.0:
+            out[lo:hi] *= np.float32(scale)
 
     list(pool.map(fill, range(len(kids))))
     return out.reshape(shape)
@@ -188,7 +195,7 @@ def gen_tensor(m: ModelShape, name: str, seed: int = 1, init: str = "paper",
     try:
         role = _role(name)
         if role == "matrix":
-            x = _normal_f32(shape, seed, idx, pool) * np.float32(0.02)
+            x = _normal_f32(shape, seed, idx, pool, 0.02)
         elif init == "paper":
             x = np.full(shape, 1.0 if role == "gain" else 0.0, np.float32)
         elif init == "perturbed":
@@ -211,3 +218,10 @@ def iter_weights(m: ModelShape, seed: int = 1, init: str = "paper") -> Iterator[
 
 def gen_weights(m: ModelShape, seed: int = 1, init: str = "paper") -> Dict[str, np.ndarray]:
     return dict(iter_weights(m, seed, init))
+
+
+def gen_normal(shape, seed: int, scale: float = 1.0) -> np.ndarray:
+    """float32 N(0, scale^2) array of any size, generated on several threads
+    (deterministic in seed, independent of the thread count)."""
+    with ThreadPoolExecutor(_threads()) as pool:
+        return _normal_f32(tuple(shape), seed, 0, pool, scale)

@@ -1,0 +1,66 @@
+"""The full codec through the C ABI: lmgc_compress (serialise -> LM tables ->
+arithmetic coding, host coding overlapped with the GPU) and lmgc_decode
+(token-by-token decoding from BOS), against the oracle's container size and
+the original bytes."""
+import numpy as np
+import pytest
+
+from gpu_util import build_model, log
+from oracle import pipeline as opipe
+from oracle.forward import Model as OModel
+from paper_2409_17836_amd import binding as B
+from synth import get_workload
+from synth.configs import hex_serial
+from synth.gen import gen_values, workload_values
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(600)]
+
+
+def _roundtrip(model, om, vals, spec, batch, tag=5, dtype=np.float32):
+    import torch
+    sp = B.serial_params(spec)
+    dv = torch.from_numpy(vals).cuda()
+    buf = B.compress(model, dv, sp, batch=batch, model_tag=tag)
+    ref = opipe.compress(vals, spec, om, model_tag=tag)
+    log(f"compressed {vals.nbytes} B -> {len(buf)} B (oracle {len(ref)} B)")
+    assert abs(len(buf) - len(ref)) <= 0.005 * len(ref)
+    back = B.decode(model, buf, batch=batch, model_tag=tag, dtype=dtype)
+    assert back.tobytes() == vals.tobytes(), "not lossless"
+    with pytest.raises(B.LMGCError):
+        B.decode(model, buf, batch=batch, model_tag=tag + 1, dtype=dtype)
+    return buf
+
+
+def test_tiny_whole_workload_roundtrip():
+    w = get_workload("tiny")
+    model, host = build_model(w.model, w.weight_seed)
+    vals = workload_values(w)
+    _roundtrip(model, OModel(w.model, host), vals, w.serial, batch=48)
+    model.close()
+
+
+def test_tiny_bytes_per_group_variants():
+    w = get_workload("tiny")
+    model, host = build_model(w.model, w.weight_seed)
+    om = OModel(w.model, host)
+    vals = gen_values("laplace:1e-3", 150, 8)
+    for bpg in (0, 1, 2, 3, 8):
+        _roundtrip(model, om, vals, hex_serial(window=256, bos_id=1, bytes_per_group=bpg), batch=4)
+    model.close()
+
+
+def test_gpt2_short_roundtrip():
+    w = get_workload("gpt2")
+    model, host = build_model(w.model, w.weight_seed, "perturbed")
+    vals = workload_values(w)[:250]                          # 2250 tokens -> 3 windows
+    _roundtrip(model, OModel(w.model, host), vals, w.serial, batch=2)
+    model.close()
+
+
+def test_tinyllama_short_roundtrip():
+    w = get_workload("tinyllama")
+    model, host = build_model(w.model, w.weight_seed)
+    spec = hex_serial(window=128, bos_id=1)
+    vals = workload_values(w)[:60]                           # 540 tokens -> 5 windows
+    _roundtrip(model, OModel(w.model, host), vals, spec, batch=4)
+    model.close()

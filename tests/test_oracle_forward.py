@@ -247,3 +247,13 @@ def test_incremental_equals_full(shape):
     inc = np.stack([lm.step(x[:, j]) for j in range(11)], 1)
     full = np.stack([model.logits(x[b]) for b in range(3)])
     np.testing.assert_allclose(inc, full, rtol=0, atol=1e-11)
+
+
+@pytest.mark.parametrize("shape", [MINI_LLAMA, MINI_GPT2])
+def test_batched_windows_equal_single_windows(shape):
+    w = gen_weights(shape, seed=8, init="perturbed")
+    model = F.Model(shape, w)
+    x = np.random.default_rng(8).integers(0, shape.vocab, (3, 9))
+    batched = model.logits(x)
+    for b in range(3):
+        np.testing.assert_allclose(batched[b], model.logits(x[b]), rtol=0, atol=1e-12)
