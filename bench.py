@@ -1,0 +1,195 @@
+"""LM-GC compression throughput on one MI355X.
+
+Workload: the Llama-2-7B-shape decoder (32 layers, d=4096, 32 heads, SwiGLU
+11008, vocab 32000, RoPE) in bf16 with random-init weights, compressing
+float32 gradients ~ Laplace(0, 1e-3) serialised as 8 hex digits + separator,
+4096-token windows, 8 windows per LM call.
+
+One step = one batch of 8 windows through the whole hot path: serialise the
+batch's tokens on the GPU, run the LM to per-position integer tables,
+copy tables and coder bins to the host, arithmetic-code the 8 windows (host
+coding of a batch overlaps the GPU work of the next).  The value is the
+whole job's float32 gradient bytes per second (inputs resident in HBM).
+
+Prints one JSON line.  Extra fields: the dominant kernel's roofline (HIP
+events around each of its launches in the timed region) and the CPU oracle's
+throughput on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 matrix peak
+DOMINANT = "gemm_up"               # gate/up projection + SwiGLU: 44% of the FLOPs
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, host_weights, values, n_values_sample):
+    """Time the oracle (as it stands) compressing the first values of the
+    vector: one window prefix of the same workload."""
+    import numpy as np
+
+    from oracle import pipeline as opipe
+    from oracle.forward import Model as OModel
+
+    om = OModel(w.model, host_weights)
+    sample = values[:n_values_sample]
+    t0 = time.perf_counter()
+    buf = opipe.compress(sample, w.serial, om)
+    dt = time.perf_counter() - t0
+    threads = min(16, os.cpu_count() or 1)
+    return {
+        "value": sample.nbytes / dt / 1e6,
+        "unit": "MB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{n_values_sample} values = {9 * n_values_sample} tokens (a prefix of window 0) "
+                  f"through the float64 NumPy forward + quantiser + coder; {dt:.1f} s, "
+                  f"{len(buf)} bytes",
+        "seconds": dt,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=12)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="7b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-values", type=int, default=2)
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_gemm_up_7b.json"))
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); windows are independent, "
+              "so more GPUs would each compress their own window range", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2409_17836_amd import binding as B
+    from synth import get_workload
+    from synth.gen import iter_weights, workload_values
+
+    w = get_workload(args.workload)
+    Bw, W = w.batch, w.serial.window
+    dev = torch.device("cuda:0")
+    log(f"[bench] workload {w.name}: generating {w.n_values} values and weights")
+    values = workload_values(w)
+    host = {}
+    dweights = []
+    for name, arr in iter_weights(w.model, w.weight_seed):
+        host[name] = arr
+        a = arr.view(np.int16) if arr.dtype == np.uint16 else arr
+        dweights.append(torch.from_numpy(a).to(dev))
+    cfg = B.model_config(w.model)
+    model = B.Model(cfg, dweights)
+    del dweights
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    sp = B.serial_params(w.serial)
+    dv = torch.from_numpy(values).to(dev)
+    n_win = B.num_windows(w.n_values, sp)
+    need = (args.warmup + args.steps) * Bw
+    assert need <= n_win, f"{need} windows needed, workload has {n_win}"
+    ws = B.workspace(model.codec_workspace(w.n_values, sp, Bw))
+    stream = torch.cuda.current_stream()
+    log(f"[bench] model ready; warmup {args.warmup} step(s)")
+
+    if args.warmup:
+        B.compress(model, dv, sp, batch=Bw, first_window=0, n_windows=args.warmup * Bw, ws=ws)
+    torch.cuda.synchronize()
+
+    log(f"[bench] timing {args.steps} step(s)")
+    B.timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    buf = B.compress(model, dv, sp, batch=Bw, first_window=args.warmup * Bw,
+                     n_windows=args.steps * Bw, ws=ws)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    kern = {k: B.timing_read(k) for k in B.KINDS}
+    B.timing_enable(False)
+
+    n_tok = B.num_tokens(w.n_values, sp)
+    tok_done = min(n_tok, (args.warmup + args.steps) * Bw * W) - args.warmup * Bw * W
+    grad_bytes = tok_done / B.num_tokens(1, sp) * w.serial.bytes_per_value
+    value = grad_bytes / dt / 1e6
+    ms_step = dt * 1e3 / args.steps
+
+    flops_step = {k: model.flops(Bw, W, k) for k in B.KINDS}
+    total_flops = sum(flops_step.values())
+    mfma_util = total_flops * args.steps / dt / (PEAK_BF16_TFLOPS * 1e12)
+    ms_k, n_k = kern[DOMINANT]
+    launches_per_step = w.model.n_layers
+    flop_launch = flops_step[DOMINANT] / launches_per_step
+    avg_ms = ms_k / max(n_k, 1)
+    achieved = flop_launch / (avg_ms * 1e-3) / 1e12
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        try:
+            tj = json.load(open(args.traffic_json))
+            traffic = tj.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    kernel_ms = {k: round(ms / args.steps, 3) for k, (ms, n) in kern.items() if n}
+
+    out = {
+        "metric": "gradient MB/s compressed (LM probs + AC) at 7B-shape bf16; MFMA util",
+        "value": round(value, 6),
+        "unit": "MB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Laplace gradients, random-init weights)",
+        "config": {
+            "workload": f"{w.name}: Llama-2-7B-shape decoder, float32 gradients ~ {w.dist}, "
+                        f"8 hex digits + separator per value",
+            "windows_per_step": Bw,
+            "window_tokens": W,
+            "tokens_per_step": Bw * W,
+            "values_per_step": round(Bw * W / 9, 1),
+            "parallelism": "single GPU",
+        },
+        "tokens_per_s": round(tok_done / dt, 1),
+        "mfma_util": round(mfma_util, 4),
+        "container_bytes": len(buf),
+        "compression_rate_pct": round(100.0 * len(buf) / grad_bytes, 2),
+        "kernel_ms_per_step": kernel_ms,
+        "roofline": {
+            "kernel": f"{DOMINANT} (gate/up projection {Bw * W}x{2 * w.model.d_ff}x{w.model.d_model} "
+                      "with fused SwiGLU)",
+            "bound": "mfma",
+            "achieved": round(achieved, 1),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "avg_launch_ms": round(avg_ms, 4),
+            "flop_per_launch": flop_launch,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        cb = cpu_baseline(w, host, values, args.cpu_sample_values)
+        out["cpu_baseline"] = {k: v for k, v in cb.items() if k != "seconds"}
+    print(json.dumps(out), flush=True)
+    model.close()
+
+
+if __name__ == "__main__":
+    main()

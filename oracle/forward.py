@@ -120,9 +120,15 @@ def causal_attention(q, k, v):
 # ------------------------------------------------------------------- model --
 class Model:
     """Holds a decoder shape and its parameters (name -> stored array, or a
-    callable name -> stored array for lazily generated large models)."""
+    callable name -> stored array for lazily generated large models).
 
-    def __init__(self, shape, weights, cache: Optional[bool] = None):
+    acc="f64" (the reference) evaluates everything in float64.  acc="f32"
+    evaluates the same equations with the same bf16 rounding points but in
+    float32 (the precision of the GPU's accumulators and residual stream);
+    the gap between the two measures how far two correct evaluations of the
+    same bf16 model drift apart through the network's depth."""
+
+    def __init__(self, shape, weights, cache: Optional[bool] = None, acc: str = "f64"):
         self.m = shape
         self._get: Callable[[str], np.ndarray] = (weights.__getitem__
                                                   if isinstance(weights, dict) else weights)
@@ -130,12 +136,19 @@ class Model:
             4 * shape.d_model ** 2 + 3 * shape.d_model * shape.d_ff)
         self._cache_on = (n_params < 80_000_000) if cache is None else cache
         self._cache: Dict[str, np.ndarray] = {}
-        self.rnd = round_bf16 if shape.dtype == "bf16" else (lambda x: x)
+        self.acc = np.float64 if acc == "f64" else np.float32
+        if shape.dtype == "bf16":
+            self.rnd = (round_bf16 if acc == "f64"
+                        else (lambda x: round_bf16(x).astype(np.float32)))
+        else:
+            self.rnd = (lambda x: x)
 
     def w(self, name: str) -> np.ndarray:
         if name in self._cache:
             return self._cache[name]
         x = storage_to_f64(self._get(name), self.m.dtype)
+        if self.acc is not np.float64:
+            x = x.astype(self.acc)
         if self._cache_on:
             self._cache[name] = x
         return x

@@ -2,7 +2,16 @@
 init): the benchmark launch configuration on the GPU, checked against the
 oracle on sampled positions (window prefixes, which causality makes exact
 sub-problems), plus determinism / prefix invariance at full size and a
-lossless round trip of a short vector through the 7B-shape model."""
+lossless round trip of a short vector through the 7B-shape model.
+
+Tolerance for these deep bf16 models: two correct evaluations of the same
+bf16 model that differ only in accumulation precision (the oracle in float64
+and in float32, identical bf16 rounding points) already disagree by more
+than 2e-2 at 22-32 layers, because a one-ulp difference in where a value
+rounds to bf16 is amplified with depth.  The test measures that floor on the
+very positions it checks and requires the GPU to stay within twice it (and
+within 2e-2 where the floor is lower), and the code length of the checked
+positions to stay within 0.5% of the oracle's."""
 import numpy as np
 import pytest
 
@@ -18,7 +27,7 @@ from synth.gen import gen_values, workload_values
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 
 
-def _parity(w, model, om, n_win, check_windows, P):
+def _parity(w, model, om, om32, n_win, check_windows, P):
     import torch
     vals = workload_values(w)
     sp = B.serial_params(w.serial)
@@ -30,12 +39,29 @@ def _parity(w, model, om, n_win, check_windows, P):
     otok, _ = opipe.serialize(vals, w.serial)
     W = w.serial.window
     X = np.stack([opipe.model_input(otok[c * W:(c + 1) * W], w.serial, P) for c in check_windows])
+    ids = opipe.alphabet_ids(w.serial)
     log(f"{w.name}: oracle on windows {check_windows} x {P} positions")
-    ref = om.alphabet_logprobs(X, opipe.alphabet_ids(w.serial))
+    ref = om.alphabet_logprobs(X, ids)
+    log(f"{w.name}: oracle (float32 accumulation) on the same positions")
+    ref32 = om32.alphabet_logprobs(X, ids)
+    floor = np.abs(ref32 - ref)
     d = np.abs(lp[check_windows, :P] - ref)
-    log(f"{w.name}: max |lp - oracle| = {d.max():.3g}, mean {d.mean():.3g}")
-    assert d.max() <= 2e-2
-    assert np.array_equal(cdf.cpu().numpy().view(np.uint32), ocoder.quantize(lp))
+    log(f"{w.name}: max |lp - oracle| = {d.max():.3g}, mean {d.mean():.3g}; oracle f32-vs-f64 "
+        f"floor max {floor.max():.3g}, mean {floor.mean():.3g}")
+    assert d.max() <= max(2e-2, 2 * floor.max())
+    assert d.mean() <= max(5e-3, 2 * floor.mean())
+    gcdf = cdf.cpu().numpy().view(np.uint32)
+    assert np.array_equal(gcdf, ocoder.quantize(lp))
+    # code length of the checked positions with the GPU's and the oracle's tables
+    _, osym = opipe.serialize(vals, w.serial)
+    sym = np.stack([osym[c * W:c * W + P] for c in check_windows]).astype(np.int64)
+    ocdf = ocoder.quantize(ref.astype(np.float32)).astype(np.int64)
+    g = gcdf[check_windows, :P].astype(np.int64)
+    take = lambda c, k: np.take_along_axis(c, k[..., None], -1)[..., 0]
+    bits_gpu = -np.log2((take(g, sym + 1) - take(g, sym)) / 65536.0).sum()
+    bits_ref = -np.log2((take(ocdf, sym + 1) - take(ocdf, sym)) / 65536.0).sum()
+    log(f"{w.name}: code length of checked positions {bits_gpu:.1f} bits vs oracle {bits_ref:.1f}")
+    assert abs(bits_gpu - bits_ref) <= 0.005 * bits_ref
     return sp, tok, cdf, logp
 
 
@@ -43,7 +69,7 @@ def test_tinyllama_launch_config():
     w = get_workload("tinyllama")
     log("tinyllama: building model")
     model, host = build_model(w.model, w.weight_seed, "perturbed")
-    _parity(w, model, OModel(w.model, host), 16, [0, 9], 96)
+    _parity(w, model, OModel(w.model, host), OModel(w.model, host, acc="f32"), 16, [0, 9], 96)
     model.close()
 
 
@@ -52,14 +78,14 @@ def llama7b():
     w = get_workload("7b")
     log("7b: building model (6.7e9 parameters)")
     model, host = build_model(w.model, w.weight_seed, "paper")
-    yield w, model, OModel(w.model, host)
+    yield w, model, OModel(w.model, host), OModel(w.model, host, acc="f32")
     model.close()
 
 
 def test_7b_launch_config_parity_and_invariance(llama7b):
     import torch
-    w, model, om = llama7b
-    sp, tok, cdf, logp = _parity(w, model, om, w.batch, [0, 7], 12)
+    w, model, om, om32 = llama7b
+    sp, tok, cdf, logp = _parity(w, model, om, om32, w.batch, [0, 7], 12)
     # the same launch again is bitwise identical; a changed suffix leaves the
     # prefix bitwise identical
     j = 3000
@@ -79,7 +105,7 @@ def test_7b_lossy_roundtrip_short(llama7b):
     """8-bit indices (2 hex digits + separator), short windows: compress with
     the library, decode token by token with the library, compare bytes."""
     import torch
-    w, model, om = llama7b
+    w, model, om, _ = llama7b
     spec = hex_serial(window=64, bos_id=1, bytes_per_value=1)
     vals = gen_values("topk_q8:1e-3:0.1", 100, 3)             # 300 tokens -> 5 windows
     sp = B.serial_params(spec)
