@@ -269,17 +269,19 @@ int lmgc_container_info(const uint8_t* container, size_t bytes, int64_t* n_value
  * C[M, N] (float32) = A[M, K] * B[N, K]^T with bfloat16 A, B (bit patterns)
  * and float32 accumulation: the matrix-product kernel of the decoder's
  * projections (Sec. 4.1 LLMs), exposed for parity tests at full size.
- * K must be a multiple of 64.  GPU, async.
+ * K must be a multiple of 64 and N of 256; A is [M, K] row-major, B is
+ * [N, K] row-major, C is [M, N] row-major.  GPU, async.
  */
 int lmgc_op_gemm_bf16(const uint16_t* d_a, const uint16_t* d_b, float* d_c, int32_t M,
                       int32_t N, int32_t K, void* stream);
 
 /*
- * Causal attention kernel on bfloat16 operands: q [B, Hq, W, hd],
- * k [B, Hkv, W, hd], vt [B, Hkv, hd, W] (v transposed) -> o [B*W, Hq*hd]
- * bfloat16, softmax of q.k/sqrt(hd) over keys <= query.  hd in {64, 128}.
+ * Causal attention kernel of the decoder on bfloat16 operands (the model
+ * the paper runs, Sec. 4.1): q [B, Hq, W, hd], k and v [B, Hkv, W, hd] ->
+ * o [B*W, Hq*hd] bfloat16, softmax of q.k/sqrt(hd) over keys <= query; query
+ * head h reads kv head h*Hkv/Hq.  hd in {64, 128}, W % 8 == 0.  GPU, async.
  */
-int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_vt,
+int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_v,
                            uint16_t* d_o, int32_t B, int32_t Hq, int32_t Hkv, int32_t W,
                            int32_t hd, void* stream);
 

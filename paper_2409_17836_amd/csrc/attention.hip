@@ -10,9 +10,10 @@
 // registers: the row max / row sum need one cross-lane exchange (lane ^ 32)
 // instead of a 32-lane reduction.  The K rows are fed to the MFMA in a
 // permuted order so that the score registers are, without any shuffle, the
-// B operand of O^T += V^T P^T (V arrives pre-transposed from the QKV
-// projection epilogue).  Softmax statistics are float32 in base 2; P is
-// rounded to bf16 for the second product; O is normalised at the end.
+// B operand of O^T += V^T P^T; V is transposed on its way into LDS.  The
+// next K/V tile is fetched into registers while the current one is in use.
+// Softmax statistics are float32 in base 2; P is rounded to bf16 for the
+// second product; O is normalised at the end.
 //
 // Determinism / prefix invariance: a query's key tiles are processed in a
 // fixed order that depends only on the query's 128-query block; masked keys
@@ -27,8 +28,9 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ inline bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ inline bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // Swizzle of the 16-byte chunks of a K row so that the 8 rows one group of
 // lanes reads together (keys {0-3, 8-11} + 16 j and {4-7, 12-15} + 16 j)
@@ -38,19 +40,28 @@ __device__ inline int kswz(int key) { return (key & 3) | ((key >> 1) & 4); }
 // key held by score register r of a lane in half h (see the S^T layout).
 __device__ inline int key_of_reg(int r, int h) { return r < 8 ? 8 * h + r : 16 + 8 * h + (r - 8); }
 
+__device__ inline uint32_t word_of(const u32x4& v, int w) { return v[w]; }
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
 __device__ inline uint32_t pack2(float a, float b) {
-  return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+  const bf16x2 v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
-                                                           const uint16_t* __restrict__ vt,
+                                                           const uint16_t* __restrict__ v,
                                                            uint16_t* __restrict__ o, int Hq,
                                                            int Hkv, int W, float sl2) {
   constexpr int BQ = 128, BKV = 64, KCH = HD / 8, NKS = HD / 16, NOB = HD / 32;
-  __shared__ uint4 sK[BKV * KCH];
-  __shared__ uint4 sV[HD * 8];
+  // per thread and tile: K chunks (16 B) and V key pairs x 8 dims
+  constexpr int NKL = BKV * KCH / 256;       // K chunks per thread
+  constexpr int NVL = (BKV / 2) * KCH / 256;  // V (key pair, dim chunk) units per thread
+  __shared__ u32x4 sK[BKV * KCH];
+  __shared__ u32x4 sV[HD * 8];  // V^T: [dim][64 keys], 16-byte chunks swizzled by dim
 
   const int nqb = (W + BQ - 1) / BQ;
   const int qb = nqb - 1 - (int)blockIdx.x;  // longest blocks first
@@ -63,14 +74,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
 
   const uint16_t* Qp = q + (int64_t)(b * Hq + h) * W * HD;
   const uint16_t* Kp = k + (int64_t)(b * Hkv + kvh) * W * HD;
-  const uint16_t* Vp = vt + (int64_t)(b * Hkv + kvh) * HD * W;
+  const uint16_t* Vp = v + (int64_t)(b * Hkv + kvh) * W * HD;
 
   bf16x8 qf[NKS];
   {
     const int qr = min(myq, W - 1);
 #pragma unroll
     for (int ks = 0; ks < NKS; ks++)
-      qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(Qp + (int64_t)qr * HD + 16 * ks + 8 * half));
+      qf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(Qp + (int64_t)qr * HD + 16 * ks + 8 * half));
   }
   f32x16 oacc[NOB];
 #pragma unroll
@@ -82,37 +93,58 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   const int pa = c32 >> 3, pg = (c32 >> 2) & 1, pc = c32 & 3;
   const int kperm = 16 * (pa >> 1) + 8 * pg + 4 * (pa & 1) + pc;
 
+  // register staging of one K/V tile (loaded one tile ahead)
+  u32x4 rk[NKL], rv[NVL][2];
+  auto gload = [&](int k0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NKL; i++) {
+      const int c = tid + 256 * i, key = c / KCH, ch = c % KCH;
+      rk[i] = *reinterpret_cast<const u32x4*>(Kp + (int64_t)min(k0 + key, W - 1) * HD + ch * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < NVL; i++) {
+      const int u = tid + 256 * i, kp = u & 31, ch = u >> 5;
+#pragma unroll
+      for (int e = 0; e < 2; e++) {
+        const int key = k0 + 2 * kp + e;
+        rv[i][e] = key < W ? *reinterpret_cast<const u32x4*>(Vp + (int64_t)key * HD + ch * 8)
+                           : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+  auto lstore = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NKL; i++) {
+      const int c = tid + 256 * i, key = c / KCH, ch = c % KCH;
+      sK[key * KCH + (ch ^ kswz(key))] = rk[i];
+    }
+    // V^T: word (dim, key pair) <- (V[2kp][dim], V[2kp+1][dim])
+    uint32_t* sv = reinterpret_cast<uint32_t*>(sV);
+#pragma unroll
+    for (int i = 0; i < NVL; i++) {
+      const int u = tid + 256 * i, kp = u & 31, ch = u >> 5;
+#pragma unroll
+      for (int e = 0; e < 8; e++) {
+        const int d = ch * 8 + e;
+        const uint32_t wa = word_of(rv[i][0], e >> 1), wb = word_of(rv[i][1], e >> 1);
+        const uint32_t lo = (e & 1) ? (wa >> 16) : (wa & 0xffffu);
+        const uint32_t hi = (e & 1) ? (wb >> 16) : (wb & 0xffffu);
+        const int kc = kp >> 2;  // 16-byte chunk of the 64-key row
+        sv[(d * 8 + (kc ^ (d & 7))) * 4 + (kp & 3)] = lo | (hi << 16);
+      }
+    }
+  };
+
   const int kend = min(W, qb * BQ + BQ);
   const int ntiles = (kend + BKV - 1) / BKV;
+  gload(0);
   for (int t = 0; t < ntiles; t++) {
     const int k0 = t * BKV;
+    __syncthreads();  // every wave is done with the previous tile
+    lstore();
     __syncthreads();
-    for (int c = tid; c < BKV * KCH; c += 256) {
-      const int key = c / KCH, ch = c % KCH;
-      const int kk = min(k0 + key, W - 1);
-      sK[key * KCH + (ch ^ kswz(key))] =
-          *reinterpret_cast<const uint4*>(Kp + (int64_t)kk * HD + ch * 8);
-    }
-    for (int c = tid; c < HD * 8; c += 256) {
-      const int d = c >> 3, ch = c & 7;
-      const int key = k0 + ch * 8;
-      const uint16_t* src = Vp + (int64_t)d * W + key;
-      uint4 val;
-      if (key + 8 <= W) {
-        val = *reinterpret_cast<const uint4*>(src);
-      } else {
-        uint16_t e[8];
-#pragma unroll
-        for (int i = 0; i < 8; i++) e[i] = (key + i < W) ? src[i] : (uint16_t)0;
-        val.x = e[0] | ((uint32_t)e[1] << 16);
-        val.y = e[2] | ((uint32_t)e[3] << 16);
-        val.z = e[4] | ((uint32_t)e[5] << 16);
-        val.w = e[6] | ((uint32_t)e[7] << 16);
-      }
-      sV[d * 8 + (ch ^ (d & 7))] = val;
-    }
-    __syncthreads();
-    if (k0 > q0 + 31) continue;  // tile entirely after this wave's queries
+    if (t + 1 < ntiles) gload(k0 + BKV);  // in flight during this tile's math
+    if (k0 > q0 + 31) continue;           // tile entirely after this wave's queries
 
     f32x16 s0 = f32x16{}, s1 = f32x16{};
 #pragma unroll
@@ -125,21 +157,22 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
       s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[ks], s1, 0, 0, 0);
     }
     float mx = -INFINITY;
+    const bool diag = k0 + BKV - 1 > q0;  // some key of the tile may lie after a query
 #pragma unroll
     for (int r = 0; r < 16; r++) {
       const int key = k0 + key_of_reg(r, half);
-      s0[r] = (key <= myq) ? s0[r] * sl2 : -INFINITY;
-      s1[r] = (key + 32 <= myq) ? s1[r] * sl2 : -INFINITY;
+      s0[r] = (!diag || key <= myq) ? s0[r] * sl2 : -INFINITY;
+      s1[r] = (!diag || key + 32 <= myq) ? s1[r] * sl2 : -INFINITY;
       mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
     }
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float mnew = fmaxf(m_i, mx);
-    const float alpha = exp2f(m_i - mnew);
+    const float alpha = __builtin_amdgcn_exp2f(m_i - mnew);
     float ls = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; r++) {
-      s0[r] = exp2f(s0[r] - mnew);
-      s1[r] = exp2f(s1[r] - mnew);
+      s0[r] = __builtin_amdgcn_exp2f(s0[r] - mnew);
+      s1[r] = __builtin_amdgcn_exp2f(s1[r] - mnew);
       ls += s0[r] + s1[r];
     }
     ls += __shfl_xor(ls, 32, 64);
@@ -153,11 +186,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
     for (int kk = 0; kk < 4; kk++) {
       const f32x16& sv = (kk < 2) ? s0 : s1;
       const int r0 = (kk & 1) * 8;
-      uint4 u;
-      u.x = pack2(sv[r0 + 0], sv[r0 + 1]);
-      u.y = pack2(sv[r0 + 2], sv[r0 + 3]);
-      u.z = pack2(sv[r0 + 4], sv[r0 + 5]);
-      u.w = pack2(sv[r0 + 6], sv[r0 + 7]);
+      const u32x4 u = {pack2(sv[r0 + 0], sv[r0 + 1]), pack2(sv[r0 + 2], sv[r0 + 3]),
+                       pack2(sv[r0 + 4], sv[r0 + 5]), pack2(sv[r0 + 6], sv[r0 + 7])};
       pf[kk] = as_bf16x8(u);
     }
 #pragma unroll
@@ -247,16 +277,16 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 
 }  // namespace
 
-hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
+hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  uint16_t* o, int B, int Hq, int Hkv, int W, int hd,
                                  hipStream_t s) {
   if (B <= 0 || W <= 0) return hipSuccess;
   const dim3 grid((W + 127) / 128, Hq, B), block(256);
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)hd));
   if (hd == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2);
+    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, sl2);
   else if (hd == 64)
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2);
+    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, sl2);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

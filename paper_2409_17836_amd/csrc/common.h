@@ -45,8 +45,7 @@ struct EpiArgs {
   float* c;            // [M, ldc]
   int ldc;
   const void* bias;    // [N] model dtype, nullable
-  // attention layout scatter: q [B,Hq,W,hd], k [B,Hkv,W,hd],
-  // v [B,Hkv,hd,W] (bf16 models, transposed) or [B,Hkv,W,hd] (f32 models)
+  // attention layout scatter: q [B,Hq,W,hd], k and v [B,Hkv,W,hd]
   void* q;
   void* k;
   void* v;
@@ -76,7 +75,7 @@ hipError_t launch_gemm_bf16(const uint16_t* A, const uint16_t* B, int M, int N_p
 hipError_t launch_gemm_f32(const float* A, const float* B, int M, int N_pad, int K,
                            const EpiArgs& e, hipStream_t s);
 
-hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
+hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  uint16_t* o, int B, int Hq, int Hkv, int W, int hd,
                                  hipStream_t s);
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,

@@ -98,7 +98,7 @@ __global__ void norm_kernel(const float* __restrict__ h, int M, int d, const voi
     float t = (v[i] - mean) * r * load_param(g, c, dtype);
     if (layernorm) t += load_param(b, c, dtype);
     if (dtype == LMGC_DTYPE_BF16)
-      ((uint16_t*)y)[row * d + c] = f32_to_bf16(t);
+      ((__bf16*)y)[row * d + c] = (__bf16)t;
     else
       ((float*)y)[row * d + c] = t;
   }

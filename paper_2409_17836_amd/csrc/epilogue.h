@@ -4,6 +4,9 @@
 //   - q/k projections: the two halves of a RoPE rotation pair (i, i + hd/2);
 //   - gate/up projection: gate and up of the same FFN feature;
 //   - everything else: two independent columns.
+// Per-column decoding (which of q/k/v, head, dim, bias) is done once per
+// column pair (Epi::column); the per-row part (Epi::row) only needs the
+// window index b and position pos of the row.
 #pragma once
 
 #include <math.h>
@@ -16,7 +19,7 @@ template <typename T>
 __device__ inline void store_act(void* p, int64_t i, float v);
 template <>
 __device__ inline void store_act<uint16_t>(void* p, int64_t i, float v) {
-  ((uint16_t*)p)[i] = f32_to_bf16(v);
+  ((__bf16*)p)[i] = (__bf16)v;  // round to nearest even (v_cvt_pk_bf16_f32)
 }
 template <>
 __device__ inline void store_act<float>(void* p, int64_t i, float v) {
@@ -35,104 +38,116 @@ __device__ inline float load_par<float>(const void* p, int i) {
   return ((const float*)p)[i];
 }
 
-__device__ inline float silu_f(float x) { return x / (1.0f + expf(-x)); }
+// silu(x) = x / (1 + e^-x) in float32 with the hardware exp2 and reciprocal
+// (about 1 ulp each); the tanh form of GELU.
+__device__ inline float silu_f(float x) {
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
+}
 
 __device__ inline float gelu_tanh_f(float x) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
   return 0.5f * x * (1.0f + tanhf(k0 * (x + 0.044715f * x * x * x)));
 }
 
-// Where a column of the fused QKV output goes: segment (0 q, 1 k, 2 v), head, dim.
-// q and k columns of a 64-column group g hold rotation pairs g*32 .. g*32+31:
-// column g*64 + t is dim i of pair P = g*32 + t, column g*64 + 32 + t its
-// partner dim i + hd/2 (head = P / (hd/2), i = P % (hd/2)).
-__device__ inline void qkv_rope_target(int col, int Hq, int Hkv, int hd, int& seg, int& head,
-                                       int& i) {
-  const int segq = Hq * hd, segk = Hkv * hd;
-  int cc = col;
-  seg = 0;
-  if (cc >= segq) {
-    cc -= segq;
-    seg = 1;
-    if (cc >= segk) {
-      cc -= segk;
-      seg = 2;
-    }
-  }
-  if (seg == 2) {  // v: natural order
-    head = cc / hd;
-    i = cc % hd;
-    return;
-  }
-  const int P = (cc >> 6) * 32 + (cc & 31);
-  head = P / (hd / 2);
-  i = P % (hd / 2);
-}
+// Column info of one (col, col + 32) pair.
+struct ColInfo {
+  int seg, head, i;     // QKV target of col: segment (0 q, 1 k, 2 v), head, dim
+  int seg2, head2, i2;  // QKV target of col + 32 (v and unrotated layouts)
+  float blo, bhi;       // biases of col and col + 32 (0 if none)
+  bool valid;
+};
 
-template <typename T, int KIND>
-__device__ inline void epi_pair(const EpiArgs& e, int row, int col, float vlo, float vhi) {
-  if (KIND != EPI_STORE_F32 && col + 32 >= e.N + 32) return;  // padded columns
-  if (KIND == EPI_STORE_F32) {
-    float* c = e.c + (int64_t)row * e.ldc;
-    if (col < e.N) c[col] = vlo;
-    if (col + 32 < e.N) c[col + 32] = vhi;
-  } else if (KIND == EPI_RESID) {
-    float* c = e.c + (int64_t)row * e.ldc;
-    if (e.bias) {
-      vlo += load_par<T>(e.bias, col);
-      vhi += load_par<T>(e.bias, col + 32);
+// HD = head dim when known at compile time (0: read e.hd).
+template <typename T, int KIND, int HD>
+struct Epi {
+  __device__ static inline int hdim(const EpiArgs& e) { return HD ? HD : e.hd; }
+
+  __device__ static inline ColInfo column(const EpiArgs& e, int col) {
+    ColInfo c;
+    c.valid = col < e.N;
+    c.seg = c.head = c.i = c.seg2 = c.head2 = c.i2 = 0;
+    c.blo = c.bhi = 0.f;
+    if (!c.valid) return c;
+    const int h = hdim(e);
+    if ((KIND == EPI_RESID || KIND == EPI_BIAS_GELU || KIND == EPI_QKV_BIAS) && e.bias) {
+      c.blo = load_par<T>(e.bias, col);
+      c.bhi = load_par<T>(e.bias, col + 32);
     }
-    c[col] += vlo;
-    c[col + 32] += vhi;
-  } else if (KIND == EPI_SWIGLU) {
-    const int f = (col >> 6) * 32 + (col & 31);
-    store_act<T>(e.out, (int64_t)row * e.ld_out + f, silu_f(vlo) * vhi);
-  } else if (KIND == EPI_BIAS_GELU) {
-    const int64_t base = (int64_t)row * e.ld_out;
-    store_act<T>(e.out, base + col, gelu_tanh_f(vlo + load_par<T>(e.bias, col)));
-    store_act<T>(e.out, base + col + 32, gelu_tanh_f(vhi + load_par<T>(e.bias, col + 32)));
-  } else if (KIND == EPI_QKV_ROPE) {
-    const int b = row / e.W, pos = row - b * e.W;
-    int seg, head, i;
-    qkv_rope_target(col, e.Hq, e.Hkv, e.hd, seg, head, i);
-    if (seg < 2) {
-      const float2 cs = e.rope[pos * (e.hd / 2) + i];
-      const float lo = vlo * cs.x - vhi * cs.y;
-      const float hi = vhi * cs.x + vlo * cs.y;
-      const int H = seg == 0 ? e.Hq : e.Hkv;
-      void* dst = seg == 0 ? e.q : e.k;
-      const int64_t base = (((int64_t)b * H + head) * e.W + pos) * e.hd;
-      store_act<T>(dst, base + i, lo);
-      store_act<T>(dst, base + i + e.hd / 2, hi);
-    } else {
-      int seg2, head2, i2;
-      qkv_rope_target(col + 32, e.Hq, e.Hkv, e.hd, seg2, head2, i2);
-      if (sizeof(T) == 2) {  // v stored transposed: [B, Hkv, hd, W]
-        store_act<T>(e.v, (((int64_t)b * e.Hkv + head) * e.hd + i) * e.W + pos, vlo);
-        store_act<T>(e.v, (((int64_t)b * e.Hkv + head2) * e.hd + i2) * e.W + pos, vhi);
-      } else {
-        store_act<T>(e.v, (((int64_t)b * e.Hkv + head) * e.W + pos) * e.hd + i, vlo);
-        store_act<T>(e.v, (((int64_t)b * e.Hkv + head2) * e.W + pos) * e.hd + i2, vhi);
+    if (KIND == EPI_QKV_ROPE) {
+      const int segq = e.Hq * h, segk = e.Hkv * h;
+      int cc = col;
+      if (cc >= segq) {
+        cc -= segq;
+        c.seg = 1;
+        if (cc >= segk) {
+          cc -= segk;
+          c.seg = 2;
+        }
       }
+      if (c.seg == 2) {  // v: natural order, the pair is (cc, cc + 32)
+        c.head = cc / h;
+        c.i = cc % h;
+        c.head2 = (cc + 32) / h;
+        c.i2 = (cc + 32) % h;
+      } else {  // 64-column group g holds rotation pairs g*32 .. g*32+31
+        const int P = (cc >> 6) * 32 + (cc & 31);
+        c.head = P / (h / 2);
+        c.i = P % (h / 2);
+      }
+    } else if (KIND == EPI_QKV_BIAS) {
+      const int d = e.Hq * h;
+      c.seg = col / d;
+      const int r = col - c.seg * d;
+      c.head = r / h;
+      c.i = r % h;
+      c.seg2 = (col + 32) / d;
+      const int r2 = col + 32 - c.seg2 * d;
+      c.head2 = r2 / h;
+      c.i2 = r2 % h;
     }
-  } else if (KIND == EPI_QKV_BIAS) {
-    const int b = row / e.W, pos = row - b * e.W;
-    const int d = e.Hq * e.hd;
-#pragma unroll
-    for (int t = 0; t < 2; t++) {
-      const int cc = col + 32 * t;
-      const float v = (t ? vhi : vlo) + load_par<T>(e.bias, cc);
-      const int seg = cc / d, r = cc - seg * d, head = r / e.hd, i = r % e.hd;
-      if (seg < 2) {
-        void* dst = seg == 0 ? e.q : e.k;
-        store_act<T>(dst, (((int64_t)b * e.Hq + head) * e.W + pos) * e.hd + i, v);
-      } else if (sizeof(T) == 2) {
-        store_act<T>(e.v, (((int64_t)b * e.Hq + head) * e.hd + i) * e.W + pos, v);
+    return c;
+  }
+
+  __device__ static inline void row(const EpiArgs& e, const ColInfo& c, int col, int rw, int b,
+                                    int pos, float vlo, float vhi) {
+    if (!c.valid) return;
+    const int h = hdim(e);
+    if (KIND == EPI_STORE_F32) {
+      float* p = e.c + (int64_t)rw * e.ldc;
+      p[col] = vlo;
+      if (col + 32 < e.N) p[col + 32] = vhi;
+    } else if (KIND == EPI_RESID) {
+      float* p = e.c + (int64_t)rw * e.ldc;
+      p[col] += vlo + c.blo;
+      p[col + 32] += vhi + c.bhi;
+    } else if (KIND == EPI_SWIGLU) {
+      const int f = (col >> 6) * 32 + (col & 31);
+      store_act<T>(e.out, (int64_t)rw * e.ld_out + f, silu_f(vlo) * vhi);
+    } else if (KIND == EPI_BIAS_GELU) {
+      const int64_t base = (int64_t)rw * e.ld_out;
+      store_act<T>(e.out, base + col, gelu_tanh_f(vlo + c.blo));
+      store_act<T>(e.out, base + col + 32, gelu_tanh_f(vhi + c.bhi));
+    } else if (KIND == EPI_QKV_ROPE) {
+      if (c.seg < 2) {
+        const float2 cs = e.rope[pos * (h / 2) + c.i];
+        const float lo = vlo * cs.x - vhi * cs.y;
+        const float hi = vhi * cs.x + vlo * cs.y;
+        const int H = c.seg == 0 ? e.Hq : e.Hkv;
+        void* dst = c.seg == 0 ? e.q : e.k;
+        const int64_t base = (((int64_t)b * H + c.head) * e.W + pos) * h;
+        store_act<T>(dst, base + c.i, lo);
+        store_act<T>(dst, base + c.i + h / 2, hi);
       } else {
-        store_act<T>(e.v, (((int64_t)b * e.Hq + head) * e.W + pos) * e.hd + i, v);
+        store_act<T>(e.v, (((int64_t)b * e.Hkv + c.head) * e.W + pos) * h + c.i, vlo);
+        store_act<T>(e.v, (((int64_t)b * e.Hkv + c.head2) * e.W + pos) * h + c.i2, vhi);
       }
+    } else if (KIND == EPI_QKV_BIAS) {
+      void* d1 = c.seg == 0 ? e.q : (c.seg == 1 ? e.k : e.v);
+      void* d2 = c.seg2 == 0 ? e.q : (c.seg2 == 1 ? e.k : e.v);
+      store_act<T>(d1, (((int64_t)b * e.Hq + c.head) * e.W + pos) * h + c.i, vlo + c.blo);
+      store_act<T>(d2, (((int64_t)b * e.Hq + c.head2) * e.W + pos) * h + c.i2, vhi + c.bhi);
     }
   }
-}
+};
 
 }  // namespace lmgc

@@ -55,12 +55,16 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
     __syncthreads();
   }
   // thread columns tx + 16 j: pairs (tx, tx + 32) and (tx + 16, tx + 48)
+  using E = Epi<float, KIND, 0>;
+  const ColInfo ci0 = E::column(e, n0 + tx), ci1 = E::column(e, n0 + tx + 16);
+  const int W = e.W > 0 ? e.W : 1;
 #pragma unroll
   for (int i = 0; i < 4; i++) {
     const int row = m0 + ty * 4 + i;
     if (row >= M) continue;
-    epi_pair<float, KIND>(e, row, n0 + tx, acc[i][0], acc[i][2]);
-    epi_pair<float, KIND>(e, row, n0 + tx + 16, acc[i][1], acc[i][3]);
+    const int b = row / W, pos = row - b * W;
+    E::row(e, ci0, n0 + tx, row, b, pos, acc[i][0], acc[i][2]);
+    E::row(e, ci1, n0 + tx + 16, row, b, pos, acc[i][1], acc[i][3]);
   }
 }
 

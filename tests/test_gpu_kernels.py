@@ -55,8 +55,7 @@ def _attn_inputs(Bn, Hq, Hkv, W, hd, seed):
 
 def _run_attn(q, k, v):
     import torch
-    vt = np.ascontiguousarray(np.swapaxes(v, 2, 3))
-    o = B.op_attention_bf16(bf16_tensor(q), bf16_tensor(k), bf16_tensor(vt))
+    o = B.op_attention_bf16(bf16_tensor(q), bf16_tensor(k), bf16_tensor(v))
     torch.cuda.synchronize()
     return o.float().cpu().numpy()
 
