@@ -277,11 +277,14 @@ int lmgc_op_gemm_bf16(const uint16_t* d_a, const uint16_t* d_b, float* d_c, int3
 
 /*
  * Causal attention kernel of the decoder on bfloat16 operands (the model
- * the paper runs, Sec. 4.1): q [B, Hq, W, hd], k and v [B, Hkv, W, hd] ->
- * o [B*W, Hq*hd] bfloat16, softmax of q.k/sqrt(hd) over keys <= query; query
- * head h reads kv head h*Hkv/Hq.  hd in {64, 128}, W % 8 == 0.  GPU, async.
+ * the paper runs, Sec. 4.1): q [B, Hq, W, hd] and k [B, Hkv, W, hd]
+ * row-major, v given TRANSPOSED as vt [B, Hkv, hd, W] (the layout the bf16
+ * decoder keeps V in) -> o [B*W, Hq*hd] bfloat16, softmax of q.k/sqrt(hd)
+ * over keys <= query; query head h reads kv head h*Hkv/Hq.  hd in {64, 128},
+ * W % 8 == 0 (else LMGC_EUNSUPPORTED).  All pointers are device memory the
+ * caller owns, 16-byte aligned.  GPU, async on `stream`.
  */
-int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_v,
+int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_vt,
                            uint16_t* d_o, int32_t B, int32_t Hq, int32_t Hkv, int32_t W,
                            int32_t hd, void* stream);
 

@@ -348,14 +348,15 @@ def op_gemm_bf16(a, b, c=None, stream=None):
     return c
 
 
-def op_attention_bf16(q, k, v, o=None, stream=None):
-    """q [B, Hq, W, hd], k and v [B, Hkv, W, hd] bf16 -> o [B*W, Hq*hd] bf16."""
+def op_attention_bf16(q, k, vt, o=None, stream=None):
+    """q [B, Hq, W, hd], k [B, Hkv, W, hd], vt = V transposed [B, Hkv, hd, W],
+    all bf16 -> o [B*W, Hq*hd] bf16."""
     import torch
     B, Hq, W, hd = q.shape
     Hkv = k.shape[1]
     if o is None:
         o = torch.empty((B * W, Hq * hd), dtype=torch.bfloat16, device=q.device)
-    _check(lib().lmgc_op_attention_bf16(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, Hq, Hkv, W, hd,
+    _check(lib().lmgc_op_attention_bf16(_ptr(q), _ptr(k), _ptr(vt), _ptr(o), B, Hq, Hkv, W, hd,
                                         _stream(stream)))
     return o
 

@@ -881,13 +881,13 @@ int lmgc_op_gemm_bf16(const uint16_t* d_a, const uint16_t* d_b, float* d_c, int3
   return LMGC_OK;
 }
 
-int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_v, uint16_t* d_o,
+int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_vt, uint16_t* d_o,
                            int32_t B, int32_t Hq, int32_t Hkv, int32_t W, int32_t hd, void* stream) {
   clear_error();
-  if (!d_q || !d_k || !d_v || !d_o || B <= 0 || W <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv)
+  if (!d_q || !d_k || !d_vt || !d_o || B <= 0 || W <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv)
     return set_error(LMGC_EINVAL, "bad arguments");
   if ((hd != 64 && hd != 128) || W % 8) return set_error(LMGC_EUNSUPPORTED, "need hd in {64, 128} and W %% 8 == 0");
-  hipError_t err = launch_attention_bf16(d_q, d_k, d_v, d_o, B, Hq, Hkv, W, hd, (hipStream_t)stream);
+  hipError_t err = launch_attention_bf16(d_q, d_k, d_vt, d_o, B, Hq, Hkv, W, hd, (hipStream_t)stream);
   if (err != hipSuccess) return set_error(LMGC_EDEVICE, "attention launch: %s", hipGetErrorString(err));
   return LMGC_OK;
 }

@@ -4,16 +4,20 @@
 // throughput lever in its discussion section).
 //
 // bf16 kernel (CDNA4 matrix cores).  A workgroup of four 64-wide waves owns
-// 128 queries of one (window, head); each wave 32 queries.  Key/value tiles
-// of 64 keys are staged in LDS.  The wave computes S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16, so each lane holds one query's scores in its own
-// registers: the row max / row sum need one cross-lane exchange (lane ^ 32)
-// instead of a 32-lane reduction.  The K rows are fed to the MFMA in a
-// permuted order so that the score registers are, without any shuffle, the
-// B operand of O^T += V^T P^T; V is transposed on its way into LDS.  The
-// next K/V tile is fetched into registers while the current one is in use.
-// Softmax statistics are float32 in base 2; P is rounded to bf16 for the
-// second product; O is normalised at the end.
+// 128 queries of one (window, head); each wave 32 queries.  Tiles of 64 keys
+// of K [key][dim] and of V^T [dim][key] (the QKV projection writes V
+// transposed) go to LDS with direct global->LDS loads into two buffers: the
+// next tile streams in while the current one is used, with one barrier per
+// tile; each buffer is its own __shared__ array so the compiler can tell the
+// in-flight loads of one buffer from the reads of the other.  The wave
+// computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so each lane holds one
+// query's scores in its own registers: the row max / row sum need one
+// cross-lane exchange (lane ^ 32) instead of a 32-lane reduction.  The K rows
+// are fed to the MFMA in a permuted order so that the score registers are,
+// without any shuffle, the B operand of O^T += V^T P^T.  Softmax statistics
+// are float32 in base 2 (the 1/sqrt(hd) scale folded into the exponent); the
+// output is rescaled only when a query's running maximum moves; P is rounded
+// to bf16 for the second product; O is normalised at the end.
 //
 // Determinism / prefix invariance: a query's key tiles are processed in a
 // fixed order that depends only on the query's 128-query block; masked keys
@@ -29,18 +33,24 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 __device__ inline bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// Swizzle of the 16-byte chunks of a K row so that the 8 rows one group of
-// lanes reads together (keys {0-3, 8-11} + 16 j and {4-7, 12-15} + 16 j)
-// fall in distinct bank groups.
-__device__ inline int kswz(int key) { return (key & 3) | ((key >> 1) & 4); }
+// LDS swizzles.  One ds_read_b128 cycle serves 16 lanes (64 banks x 4 B =
+// 256 B), so the 16 rows such a group reads must land on 16 distinct
+// 16-byte slots modulo 256 B.
+//  - K tile [key][hd], rows of hd*2 bytes: the S^T operand lanes 0..15 read
+//    keys {0-3, 8-11, 4-7, 12-15} (+16): for hd = 128 (256-byte rows) the
+//    slot is chunk ^ (key & 15); for hd = 64 (128-byte rows) rows of equal
+//    parity share a half, so the slot is chunk ^ ((key >> 1) & 7).
+//  - V^T tile [dim][64 keys], 128-byte rows: slot = chunk ^ ((dim >> 1) & 7).
+template <int HD>
+__device__ inline int kswz(int key) { return HD == 128 ? (key & 15) : ((key >> 1) & 7); }
+__device__ inline int vswz(int d) { return (d >> 1) & 7; }
 
 // key held by score register r of a lane in half h (see the S^T layout).
 __device__ inline int key_of_reg(int r, int h) { return r < 8 ? 8 * h + r : 16 + 8 * h + (r - 8); }
-
-__device__ inline uint32_t word_of(const u32x4& v, int w) { return v[w]; }
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -53,15 +63,15 @@ __device__ inline uint32_t pack2(float a, float b) {
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
-                                                           const uint16_t* __restrict__ v,
+                                                           const uint16_t* __restrict__ vt,
                                                            uint16_t* __restrict__ o, int Hq,
                                                            int Hkv, int W, float sl2) {
   constexpr int BQ = 128, BKV = 64, KCH = HD / 8, NKS = HD / 16, NOB = HD / 32;
-  // per thread and tile: K chunks (16 B) and V key pairs x 8 dims
-  constexpr int NKL = BKV * KCH / 256;       // K chunks per thread
-  constexpr int NVL = (BKV / 2) * KCH / 256;  // V (key pair, dim chunk) units per thread
-  __shared__ u32x4 sK[BKV * KCH];
-  __shared__ u32x4 sV[HD * 8];  // V^T: [dim][64 keys], 16-byte chunks swizzled by dim
+  constexpr int KROWS = 1024 / (HD * 2);          // K rows per 1 KB direct load
+  constexpr int NKL = BKV * HD * 2 / 1024 / 4;    // direct K loads per wave and tile
+  // two LDS buffers: tile t+1 is filled while tile t is read
+  __shared__ u32x4 sK0[BKV * KCH], sK1[BKV * KCH];
+  __shared__ u32x4 sV0[HD * 8], sV1[HD * 8];  // V^T: [dim][64 keys]
 
   const int nqb = (W + BQ - 1) / BQ;
   const int qb = nqb - 1 - (int)blockIdx.x;  // longest blocks first
@@ -74,7 +84,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
 
   const uint16_t* Qp = q + (int64_t)(b * Hq + h) * W * HD;
   const uint16_t* Kp = k + (int64_t)(b * Hkv + kvh) * W * HD;
-  const uint16_t* Vp = v + (int64_t)(b * Hkv + kvh) * W * HD;
+  const uint16_t* Vp = vt + (int64_t)(b * Hkv + kvh) * HD * W;
 
   bf16x8 qf[NKS];
   {
@@ -93,113 +103,123 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   const int pa = c32 >> 3, pg = (c32 >> 2) & 1, pc = c32 & 3;
   const int kperm = 16 * (pa >> 1) + 8 * pg + 4 * (pa & 1) + pc;
 
-  // register staging of one K/V tile (loaded one tile ahead)
-  u32x4 rk[NKL], rv[NVL][2];
-  auto gload = [&](int k0) __attribute__((always_inline)) {
+  // K: direct global->LDS loads.  Load i of wave w covers tile rows
+  // (w*NKL + i)*KROWS .. +KROWS; lane l lands at row +l/KCH, slot l%KCH and
+  // fetches the chunk the swizzle puts there.
+  auto kload = [&](u32x4* sKb, int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NKL; i++) {
-      const int c = tid + 256 * i, key = c / KCH, ch = c % KCH;
-      rk[i] = *reinterpret_cast<const u32x4*>(Kp + (int64_t)min(k0 + key, W - 1) * HD + ch * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < NVL; i++) {
-      const int u = tid + 256 * i, kp = u & 31, ch = u >> 5;
-#pragma unroll
-      for (int e = 0; e < 2; e++) {
-        const int key = k0 + 2 * kp + e;
-        rv[i][e] = key < W ? *reinterpret_cast<const u32x4*>(Vp + (int64_t)key * HD + ch * 8)
-                           : u32x4{0u, 0u, 0u, 0u};
-      }
+      const int key = (wave * NKL + i) * KROWS + lane / KCH;
+      const int ch = (lane % KCH) ^ kswz<HD>(key);
+      const uint16_t* src = Kp + (int64_t)min(k0 + key, W - 1) * HD + ch * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (lds_ptr_t)(sKb + (wave * NKL + i) * 64), 16, 0, 0);
     }
   };
-  auto lstore = [&]() __attribute__((always_inline)) {
+  // V^T direct loads: HD rows (dims) x 128 B per tile = HD/8 wave loads;
+  // load i of wave w covers rows (w*NVD + i)*8 .. +8, lane l -> row +l/8, slot
+  // l%8.  W % 8 == 0, so an 8-key chunk lies wholly before or after the end
+  // of the window; chunks after it re-read the last chunk (finite values
+  // that meet probability exactly 0) so that no load leaves the row.
+  constexpr int NVD = HD * 128 / 1024 / 4;
+  auto vtload = [&](u32x4* sVb, int k0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < NKL; i++) {
-      const int c = tid + 256 * i, key = c / KCH, ch = c % KCH;
-      sK[key * KCH + (ch ^ kswz(key))] = rk[i];
-    }
-    // V^T: word (dim, key pair) <- (V[2kp][dim], V[2kp+1][dim])
-    uint32_t* sv = reinterpret_cast<uint32_t*>(sV);
-#pragma unroll
-    for (int i = 0; i < NVL; i++) {
-      const int u = tid + 256 * i, kp = u & 31, ch = u >> 5;
-#pragma unroll
-      for (int e = 0; e < 8; e++) {
-        const int d = ch * 8 + e;
-        const uint32_t wa = word_of(rv[i][0], e >> 1), wb = word_of(rv[i][1], e >> 1);
-        const uint32_t lo = (e & 1) ? (wa >> 16) : (wa & 0xffffu);
-        const uint32_t hi = (e & 1) ? (wb >> 16) : (wb & 0xffffu);
-        const int kc = kp >> 2;  // 16-byte chunk of the 64-key row
-        sv[(d * 8 + (kc ^ (d & 7))) * 4 + (kp & 3)] = lo | (hi << 16);
-      }
+    for (int i = 0; i < NVD; i++) {
+      const int d = (wave * NVD + i) * 8 + lane / 8;
+      const int ch = (lane % 8) ^ vswz(d);
+      const uint16_t* src = Vp + (int64_t)d * W + min(k0 + ch * 8, W - 8);
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (lds_ptr_t)(sVb + (wave * NVD + i) * 64), 16, 0, 0);
     }
   };
-
   const int kend = min(W, qb * BQ + BQ);
   const int ntiles = (kend + BKV - 1) / BKV;
-  gload(0);
-  for (int t = 0; t < ntiles; t++) {
+  auto tile = [&](int t, const u32x4* sKc, const u32x4* sVc, u32x4* sKn, u32x4* sVn)
+      __attribute__((always_inline)) {
     const int k0 = t * BKV;
-    __syncthreads();  // every wave is done with the previous tile
-    lstore();
+    // tile t is in (sKc, sVc); every wave is done with tile t-1, whose
+    // buffers (sKn, sVn) are refilled with tile t+1 during this tile's math
     __syncthreads();
-    if (t + 1 < ntiles) gload(k0 + BKV);  // in flight during this tile's math
-    if (k0 > q0 + 31) continue;           // tile entirely after this wave's queries
+    if (t + 1 < ntiles) {
+      kload(sKn, k0 + BKV);
+      vtload(sVn, k0 + BKV);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (k0 <= q0 + 31) {  // else the tile lies entirely after this wave's queries
+      f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+      for (int ks = 0; ks < NKS; ks++) {
+        const int ch = 2 * ks + half;
+        const int key0 = kperm, key1 = 32 + kperm;
+        const bf16x8 ka = as_bf16x8(sKc[key0 * KCH + (ch ^ kswz<HD>(key0))]);
+        const bf16x8 kb = as_bf16x8(sKc[key1 * KCH + (ch ^ kswz<HD>(key1))]);
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[ks], s1, 0, 0, 0);
+      }
+      // scores stay unscaled: p = 2^(s*sl2 - m*sl2) with m the running raw max
+      float mx = -INFINITY;
+      const bool diag = k0 + BKV - 1 > q0;  // some key of the tile may lie after a query
+      if (diag) {
+#pragma unroll
+        for (int r = 0; r < 16; r++) {
+          const int key = k0 + key_of_reg(r, half);
+          if (key > myq) s0[r] = -INFINITY;
+          if (key + 32 > myq) s1[r] = -INFINITY;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 16; r++) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mnew = fmaxf(m_i, mx);
+      const float nms = -mnew * sl2;
+      float ls = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; r++) {
+        s0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nms));
+        s1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nms));
+        ls += s0[r] + s1[r];
+      }
+      ls += __shfl_xor(ls, 32, 64);
+      if (mnew != m_i) {  // running max moved: rescale (skipped when the factor is exactly 1)
+        const float alpha = __builtin_amdgcn_exp2f((m_i - mnew) * sl2);
+        l_i *= alpha;
+#pragma unroll
+        for (int i = 0; i < NOB; i++) oacc[i] *= alpha;
+      }
+      l_i += ls;
+      m_i = mnew;
 
-    f32x16 s0 = f32x16{}, s1 = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < NKS; ks++) {
-      const int ch = 2 * ks + half;
-      const int key0 = kperm, key1 = 32 + kperm;
-      const bf16x8 ka = as_bf16x8(sK[key0 * KCH + (ch ^ kswz(key0))]);
-      const bf16x8 kb = as_bf16x8(sK[key1 * KCH + (ch ^ kswz(key1))]);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[ks], s1, 0, 0, 0);
-    }
-    float mx = -INFINITY;
-    const bool diag = k0 + BKV - 1 > q0;  // some key of the tile may lie after a query
-#pragma unroll
-    for (int r = 0; r < 16; r++) {
-      const int key = k0 + key_of_reg(r, half);
-      s0[r] = (!diag || key <= myq) ? s0[r] * sl2 : -INFINITY;
-      s1[r] = (!diag || key + 32 <= myq) ? s1[r] * sl2 : -INFINITY;
-      mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mnew = fmaxf(m_i, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_i - mnew);
-    float ls = 0.f;
-#pragma unroll
-    for (int r = 0; r < 16; r++) {
-      s0[r] = __builtin_amdgcn_exp2f(s0[r] - mnew);
-      s1[r] = __builtin_amdgcn_exp2f(s1[r] - mnew);
-      ls += s0[r] + s1[r];
-    }
-    ls += __shfl_xor(ls, 32, 64);
-    l_i = l_i * alpha + ls;
-    m_i = mnew;
-#pragma unroll
-    for (int i = 0; i < NOB; i++) oacc[i] *= alpha;
-
-    bf16x8 pf[4];
-#pragma unroll
-    for (int kk = 0; kk < 4; kk++) {
-      const f32x16& sv = (kk < 2) ? s0 : s1;
-      const int r0 = (kk & 1) * 8;
-      const u32x4 u = {pack2(sv[r0 + 0], sv[r0 + 1]), pack2(sv[r0 + 2], sv[r0 + 3]),
-                       pack2(sv[r0 + 4], sv[r0 + 5]), pack2(sv[r0 + 6], sv[r0 + 7])};
-      pf[kk] = as_bf16x8(u);
-    }
-#pragma unroll
-    for (int i = 0; i < NOB; i++) {
-      const int d = i * 32 + c32;
+      bf16x8 pf[4];
 #pragma unroll
       for (int kk = 0; kk < 4; kk++) {
-        const bf16x8 va = as_bf16x8(sV[d * 8 + ((2 * kk + half) ^ (d & 7))]);
-        oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[kk], oacc[i], 0, 0, 0);
+        const f32x16& sv = (kk < 2) ? s0 : s1;
+        const int r0 = (kk & 1) * 8;
+        const u32x4 u = {pack2(sv[r0 + 0], sv[r0 + 1]), pack2(sv[r0 + 2], sv[r0 + 3]),
+                         pack2(sv[r0 + 4], sv[r0 + 5]), pack2(sv[r0 + 6], sv[r0 + 7])};
+        pf[kk] = as_bf16x8(u);
+      }
+#pragma unroll
+      for (int i = 0; i < NOB; i++) {
+        const int d = i * 32 + c32;
+#pragma unroll
+        for (int kk = 0; kk < 4; kk++) {
+          const bf16x8 va = as_bf16x8(sVc[d * 8 + ((2 * kk + half) ^ vswz(d))]);
+          oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[kk], oacc[i], 0, 0, 0);
+        }
       }
     }
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  };
+  kload(sK0, 0);
+  vtload(sV0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  int t = 0;
+  for (; t + 2 <= ntiles; t += 2) {
+    tile(t, sK0, sV0, sK1, sV1);
+    tile(t + 1, sK1, sV1, sK0, sV0);
   }
+  if (t < ntiles) tile(t, sK0, sV0, sK1, sV1);
 
   if (myq < W) {
     const float inv = 1.0f / l_i;
@@ -277,20 +297,22 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 
 }  // namespace
 
-hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
                                  uint16_t* o, int B, int Hq, int Hkv, int W, int hd,
                                  hipStream_t s) {
   if (B <= 0 || W <= 0) return hipSuccess;
+  if (W % 8) return hipErrorInvalidValue;
   const dim3 grid((W + 127) / 128, Hq, B), block(256);
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)hd));
   if (hd == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, sl2);
+    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2);
   else if (hd == 64)
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, sl2);
+    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
+
 
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o, int B,
                                 int Hq, int Hkv, int W, int hd, hipStream_t s) {

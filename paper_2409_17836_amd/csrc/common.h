@@ -45,7 +45,8 @@ struct EpiArgs {
   float* c;            // [M, ldc]
   int ldc;
   const void* bias;    // [N] model dtype, nullable
-  // attention layout scatter: q [B,Hq,W,hd], k and v [B,Hkv,W,hd]
+  // attention layout scatter: q [B,Hq,W,hd], k [B,Hkv,W,hd]; v [B,Hkv,hd,W]
+  // (transposed) for bf16 models, [B,Hkv,W,hd] for f32 models
   void* q;
   void* k;
   void* v;
@@ -75,7 +76,7 @@ hipError_t launch_gemm_bf16(const uint16_t* A, const uint16_t* B, int M, int N_p
 hipError_t launch_gemm_f32(const float* A, const float* B, int M, int N_pad, int K,
                            const EpiArgs& e, hipStream_t s);
 
-hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
                                  uint16_t* o, int B, int Hq, int Hkv, int W, int hd,
                                  hipStream_t s);
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,

@@ -6,7 +6,9 @@
 //   - everything else: two independent columns.
 // Per-column decoding (which of q/k/v, head, dim, bias) is done once per
 // column pair (Epi::column); the per-row part (Epi::row) only needs the
-// window index b and position pos of the row.
+// window index b and position pos of the row.  bf16 models store V
+// transposed ([B, Hkv, hd, W]) for the attention kernel; Epi::rows4 writes
+// four consecutive positions of a V column as one 8-byte store.
 #pragma once
 
 #include <math.h>
@@ -138,15 +140,66 @@ struct Epi {
         store_act<T>(dst, base + c.i, lo);
         store_act<T>(dst, base + c.i + h / 2, hi);
       } else {
-        store_act<T>(e.v, (((int64_t)b * e.Hkv + c.head) * e.W + pos) * h + c.i, vlo);
-        store_act<T>(e.v, (((int64_t)b * e.Hkv + c.head2) * e.W + pos) * h + c.i2, vhi);
+        store_act<T>(e.v, vidx(e, b, e.Hkv, c.head, c.i, pos), vlo);
+        store_act<T>(e.v, vidx(e, b, e.Hkv, c.head2, c.i2, pos), vhi);
       }
     } else if (KIND == EPI_QKV_BIAS) {
-      void* d1 = c.seg == 0 ? e.q : (c.seg == 1 ? e.k : e.v);
-      void* d2 = c.seg2 == 0 ? e.q : (c.seg2 == 1 ? e.k : e.v);
-      store_act<T>(d1, (((int64_t)b * e.Hq + c.head) * e.W + pos) * h + c.i, vlo + c.blo);
-      store_act<T>(d2, (((int64_t)b * e.Hq + c.head2) * e.W + pos) * h + c.i2, vhi + c.bhi);
+      const float v1 = vlo + c.blo, v2 = vhi + c.bhi;
+      if (c.seg == 2) store_act<T>(e.v, vidx(e, b, e.Hq, c.head, c.i, pos), v1);
+      else store_act<T>(c.seg ? e.k : e.q, (((int64_t)b * e.Hq + c.head) * e.W + pos) * h + c.i, v1);
+      if (c.seg2 == 2) store_act<T>(e.v, vidx(e, b, e.Hq, c.head2, c.i2, pos), v2);
+      else store_act<T>(c.seg2 ? e.k : e.q, (((int64_t)b * e.Hq + c.head2) * e.W + pos) * h + c.i2, v2);
     }
+  }
+
+  // Element index of (window b, kv head, dim i, position pos) of V.
+  __device__ static inline int64_t vidx(const EpiArgs& e, int b, int H, int head, int i, int pos) {
+    const int h = hdim(e);
+    return sizeof(T) == 2 ? (((int64_t)b * H + head) * h + i) * e.W + pos
+                          : (((int64_t)b * H + head) * e.W + pos) * h + i;
+  }
+
+  // Rows rw0 .. rw0+3 (positions p0 .. p0+3 of window b; p0 % 4 == 0).
+  __device__ static inline void rows4(const EpiArgs& e, const ColInfo& c, int col, int rw0, int M,
+                                      int b, int p0, const float* lo, const float* hi) {
+    if (!c.valid) return;
+    constexpr bool qkv = KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS;
+    if (qkv && sizeof(T) == 2 && rw0 + 3 < M && (c.seg == 2 || c.seg2 == 2)) {
+      const int H = KIND == EPI_QKV_ROPE ? e.Hkv : e.Hq;
+      const float bl = KIND == EPI_QKV_BIAS ? c.blo : 0.f, bh = KIND == EPI_QKV_BIAS ? c.bhi : 0.f;
+      if (c.seg == 2) {
+        store4(e.v, vidx(e, b, H, c.head, c.i, p0), lo[0] + bl, lo[1] + bl, lo[2] + bl, lo[3] + bl);
+      } else {
+        for (int r = 0; r < 4; r++) row_one(e, c, col, rw0 + r, b, p0 + r, lo[r], true);
+      }
+      if (c.seg2 == 2 || (KIND == EPI_QKV_ROPE && c.seg == 2)) {
+        store4(e.v, vidx(e, b, H, c.head2, c.i2, p0), hi[0] + bh, hi[1] + bh, hi[2] + bh, hi[3] + bh);
+      } else {
+        for (int r = 0; r < 4; r++) row_one(e, c, col, rw0 + r, b, p0 + r, hi[r], false);
+      }
+      return;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; r++)
+      if (rw0 + r < M) row(e, c, col, rw0 + r, b, p0 + r, lo[r], hi[r]);
+  }
+
+ private:
+  // four consecutive bf16 values, 8-byte aligned
+  __device__ static inline void store4(void* p, int64_t idx, float a, float b, float c, float d) {
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    const bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};
+    *reinterpret_cast<bf16x4*>((uint16_t*)p + idx) = v;
+  }
+  // one half (col or col + 32) of a QKV_BIAS pair whose other half is V
+  __device__ static inline void row_one(const EpiArgs& e, const ColInfo& c, int col, int rw, int b,
+                                        int pos, float v, bool first) {
+    const int h = hdim(e);
+    const int seg = first ? c.seg : c.seg2, head = first ? c.head : c.head2, i = first ? c.i : c.i2;
+    const float bias = first ? c.blo : c.bhi;
+    store_act<T>(seg ? e.k : e.q, (((int64_t)b * e.Hq + head) * e.W + pos) * h + i, v + bias);
+    (void)col;
+    (void)rw;
   }
 };
 

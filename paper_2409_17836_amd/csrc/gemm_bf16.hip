@@ -151,14 +151,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   for (int i = 0; i < 8; i++) {
     const int r0 = m0 + wm * 128 + 16 * i + 4 * kq;
     const int b = r0 / W, p0 = r0 - b * W;
-#pragma unroll
-    for (int r = 0; r < 4; r++) {
-      const int row = r0 + r;
-      if (row < M) {
-        E::row(e, ci0, c0, row, b, p0 + r, acc[i][0][r], acc[i][2][r]);
-        E::row(e, ci1, c0 + 16, row, b, p0 + r, acc[i][1][r], acc[i][3][r]);
-      }
-    }
+    const float a0[4] = {acc[i][0][0], acc[i][0][1], acc[i][0][2], acc[i][0][3]};
+    const float a2[4] = {acc[i][2][0], acc[i][2][1], acc[i][2][2], acc[i][2][3]};
+    const float a1[4] = {acc[i][1][0], acc[i][1][1], acc[i][1][2], acc[i][1][3]};
+    const float a3[4] = {acc[i][3][0], acc[i][3][1], acc[i][3][2], acc[i][3][3]};
+    E::rows4(e, ci0, c0, r0, M, b, p0, a0, a2);
+    E::rows4(e, ci1, c0 + 16, r0, M, b, p0, a1, a3);
   }
 }
 

@@ -54,8 +54,10 @@ def _attn_inputs(Bn, Hq, Hkv, W, hd, seed):
 
 
 def _run_attn(q, k, v):
+    """v is given natural [B, Hkv, W, hd]; the kernel takes it transposed."""
     import torch
-    o = B.op_attention_bf16(bf16_tensor(q), bf16_tensor(k), bf16_tensor(v))
+    vt = np.ascontiguousarray(np.swapaxes(v, 2, 3))
+    o = B.op_attention_bf16(bf16_tensor(q), bf16_tensor(k), bf16_tensor(vt))
     torch.cuda.synchronize()
     return o.float().cpu().numpy()
 
