@@ -3,10 +3,10 @@
  * hot path: "Language Models as Zero-shot Lossless Gradient Compressors"
  * (arXiv 2409.17836).
  *
- * The method (Sec. 3): serialise float32 gradients as hexadecimal text with a
+ * The method (Sec. 4): serialise float32 gradients as hexadecimal text with a
  * separator after every 4 bytes, run a causal language model over the token
  * stream to get p(t_k | BOS, t_<k) for every token (Eq. 2), and use these
- * probabilities as the model of an arithmetic coder (Sec. 2, "Arithmetic
+ * probabilities as the model of an arithmetic coder (Sec. 3, "Arithmetic
  * coding"); decompression replays the model from BOS token by token.
  *
  * Conventions
@@ -49,8 +49,8 @@ const char* lmgc_version(void);
 
 /* ---------------------------------------------------------- serialisation */
 /*
- * Serialisation parameters (Sec. 3, "Serialization"; byte-grouping ablation
- * in Sec. 4.3).  The value vector is read as a stream of bytes, each value's
+ * Serialisation parameters (Sec. 4, "Serialization"; byte-grouping ablation
+ * in Sec. 5.3).  The value vector is read as a stream of bytes, each value's
  * bytes most-significant first when msb_first=1 (sign/exponent digits lead,
  * like printf("%08x")) or in memory (little-endian) order when msb_first=0;
  * each byte gives two hex-digit tokens, high nibble first; a separator token
@@ -166,7 +166,7 @@ void lmgc_model_destroy(lmgc_model* m);
 size_t lmgc_probs_workspace(const lmgc_model* m, int32_t B, int32_t W);
 
 /*
- * The LM as the coder's model (Sec. 3, "Compression": P_AC = P_LM).
+ * The LM as the coder's model (Sec. 4, "Compression": P_AC = P_LM).
  * d_tokens: [B, W] int32 data tokens of B windows (the BOS shift is done
  * here).  For every window b and position j < W:
  *   lp[a]  = log p(alphabet token a | BOS, tokens[b, 0..j-1]), normalised
@@ -186,7 +186,7 @@ int lmgc_probs(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t 
 
 /* ---------------------------------------------------------------- coding */
 /*
- * Arithmetic coding (Sec. 2): a Witten-Neal-Cleary binary arithmetic coder
+ * Arithmetic coding (Sec. 3): a Witten-Neal-Cleary binary arithmetic coder
  * with 62-bit code values.  Each window is an independent bitstream, packed
  * most significant bit first and padded with zero bits to a whole byte.
  * Flush: pending+1 bits, the first 0 if low < 1/4 else 1.
@@ -268,7 +268,7 @@ int lmgc_container_info(const uint8_t* container, size_t bytes, int64_t* n_value
 /*
  * C[M, N] (float32) = A[M, K] * B[N, K]^T with bfloat16 A, B (bit patterns)
  * and float32 accumulation: the matrix-product kernel of the decoder's
- * projections (Sec. 4.1 LLMs), exposed for parity tests at full size.
+ * projections (Sec. 5.1 LLMs), exposed for parity tests at full size.
  * K must be a multiple of 64 and N of 256; A is [M, K] row-major, B is
  * [N, K] row-major, C is [M, N] row-major.  GPU, async.
  */
@@ -277,7 +277,7 @@ int lmgc_op_gemm_bf16(const uint16_t* d_a, const uint16_t* d_b, float* d_c, int3
 
 /*
  * Causal attention kernel of the decoder on bfloat16 operands (the model
- * the paper runs, Sec. 4.1): q [B, Hq, W, hd] and k [B, Hkv, W, hd]
+ * the paper runs, Sec. 5.1): q [B, Hq, W, hd] and k [B, Hkv, W, hd]
  * row-major, v given TRANSPOSED as vt [B, Hkv, hd, W] (the layout the bf16
  * decoder keeps V in) -> o [B*W, Hq*hd] bfloat16, softmax of q.k/sqrt(hd)
  * over keys <= query; query head h reads kv head h*Hkv/Hq.  hd in {64, 128},

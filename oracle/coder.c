@@ -2,12 +2,12 @@
  * LM-GC reference coder -- TEST INFRASTRUCTURE ONLY.
  *
  * Plain, slow, obviously-correct C for the integer parts of LM-GC:
- *   - hex serialisation of values and its inverse      (Sec. 3, "Serialization")
+ *   - hex serialisation of values and its inverse      (Sec. 4, "Serialization")
  *   - quantisation of per-position log-probabilities
- *     into an integer frequency table / CDF             (Sec. 3, "Compression":
+ *     into an integer frequency table / CDF             (Sec. 4, "Compression":
  *                                                        the LM's distribution is
  *                                                        the coder's model)
- *   - a Witten-Neal-Cleary binary arithmetic coder      (Sec. 2, "Arithmetic coding")
+ *   - a Witten-Neal-Cleary binary arithmetic coder      (Sec. 3, "Arithmetic coding")
  *
  * Only the tests, the smoke check and the benchmark's CPU-baseline leg may load
  * this file's library.  It shares no code with the GPU library.

@@ -1,7 +1,7 @@
 """ctypes wrapper of the reference coder in coder.c -- TEST INFRASTRUCTURE ONLY.
 
-Serialisation (Sec. 3, "Serialization"), probability-table quantisation
-(Sec. 3, "Compression": P_AC = P_LM) and the arithmetic coder (Sec. 2,
+Serialisation (Sec. 4, "Serialization"), probability-table quantisation
+(Sec. 4, "Compression": P_AC = P_LM) and the arithmetic coder (Sec. 3,
 "Arithmetic coding").  See coder.c for the readings taken where the paper is
 silent.
 """

@@ -5,7 +5,7 @@ shapes LM-GC uses as priors.  Matrix products use np.matmul; everything else
 is written out.  Only the tests, the smoke check and the benchmark's
 CPU-baseline leg may use this module.
 
-Model definition (the paper only names the LLMs, Sec. 4.1; these are the
+Model definition (the paper only names the LLMs, Sec. 5.1; these are the
 standard LLaMA and GPT-2 block equations):
 
   LLaMA:  h = E[x]
@@ -227,7 +227,7 @@ class IncrementalLM:
     """Token-at-a-time evaluation with cached keys/values, batched over
     independent windows.  Used for both directions of the reference codec's
     own round trip, so that encoder and decoder compute every table with the
-    same sequence of operations (Sec. 3: decompression starts from BOS and
+    same sequence of operations (Sec. 4: decompression starts from BOS and
     feeds each decoded token back)."""
 
     def __init__(self, model: Model, nb: int, n_max: int):

@@ -3,7 +3,7 @@
 Serialise -> cut into windows -> per window: BOS-shifted model input,
 per-position log-probabilities of the 17 alphabet symbols, integer tables,
 arithmetic coding -> container.  Decompression mirrors it token by token
-(Sec. 3, "Compression").
+(Sec. 4, "Compression").
 
 Windowing reading: the serialised stream is cut into consecutive windows of
 W tokens (the last one shorter); window w's model input is BOS followed by

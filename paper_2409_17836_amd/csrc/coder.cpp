@@ -1,5 +1,5 @@
 // Host side of the LM-GC boundary: arithmetic coding of windows against the
-// per-position tables the LM produces (Sec. 2, "Arithmetic coding"; Sec. 3,
+// per-position tables the LM produces (Sec. 3, "Arithmetic coding"; Sec. 4,
 // "Compression"), the inverse of serialisation, and the container format.
 //
 // The coder is the Witten-Neal-Cleary binary arithmetic coder with 62-bit

@@ -1,5 +1,5 @@
 // Serialisation kernel: values -> hex-digit + separator token windows
-// (Sec. 3, "Serialization").  Each thread produces four consecutive tokens of
+// (Sec. 4, "Serialization").  Each thread produces four consecutive tokens of
 // the window range and stores them with one 16-byte and one 4-byte store;
 // the value bytes it needs are read through the cache (nine tokens share
 // one float32).  The work is HBM-bound: 4/9 B read and 5 B written per token.

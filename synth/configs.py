@@ -1,13 +1,13 @@
 """The five LM-GC workloads: decoder shapes, serialisation and value distributions.
 
-Decoder shapes follow the LLMs the paper uses as priors (Section 4.1: TinyLlama
+Decoder shapes follow the LLMs the paper uses as priors (Section 5.1: TinyLlama
 1.1B and LLaMA-2 7B; the GPT-2-small shape and a tiny fp32 decoder are extra
 test shapes).  Window sizes follow the paper's window ablation (Fig. 2 caption:
 256 ... 4096 tokens).  Weights are random-init, because no checkpoint is
 available; every matrix and embedding is N(0, 0.02), norm gains are 1 and
 biases are 0.
 
-Serialisation (Section 3, "Serialization"): every float32 becomes 8 hex digits
+Serialisation (Section 4, "Serialization"): every float32 becomes 8 hex digits
 (one per 4-bit partition) followed by one separator token; the tokenizer is a
 fixed one-id-per-character map (lowercase ASCII codes for the digits, 32 for
 the space separator of the H_s variant).

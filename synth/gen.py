@@ -50,7 +50,7 @@ def _topk_zero_rest(v: np.ndarray, frac: float) -> np.ndarray:
 
 
 def _linear_quantize_u8(v: np.ndarray) -> np.ndarray:
-    """Linear n=8-bit quantisation of a vector to its indices (Sec. 4.4, Eq. 4):
+    """Linear n=8-bit quantisation of a vector to its indices (Sec. 5.4, Eq. 4):
     (v - min) / (max - min) * (2^n - 1), rounded half-to-even, in float32."""
     v = v.astype(np.float32)
     mn = np.float32(v.min())

@@ -212,7 +212,7 @@ def test_roundtrip_and_length_bound(kind, T):
         payload, nbits = coder.ac_encode(cdf, sym)
         assert (coder.ac_decode(cdf, payload, nbits) == sym).all()
         H = float(-np.sum(np.log2(f[np.arange(n), sym] / T))) if n else 0.0
-        # Sec. 2: H <= l(c) <= H + 2 for one message
+        # Sec. 3: H <= l(c) <= H + 2 for one message
         assert H - 1e-6 <= nbits <= H + 2 + 1e-6
 
 

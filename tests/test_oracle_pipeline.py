@@ -31,7 +31,7 @@ def test_tiny_roundtrip_is_lossless(tiny):
 
 
 def test_code_length_matches_model_information(tiny):
-    """Per window: H <= bits <= H + 2 where H = sum of -log2 f/T (Sec. 2)."""
+    """Per window: H <= bits <= H + 2 where H = sum of -log2 f/T (Sec. 3)."""
     w, model, vals = tiny
     tok, sym = pipeline.serialize(vals[:300], w.serial)
     for s, n in pipeline.windows(tok.size, w.serial.window):
