@@ -6,14 +6,23 @@
 // per SIMD so that one wave's LDS reads and waits overlap the other's matrix
 // instructions; wave (wm, wn) owns rows wm*128 .. +128 and columns
 // wn*64 .. +64 as 8 x 4 blocks of v_mfma_f32_16x16x32_bf16.
-// K advances in steps of 64 through a double-buffered LDS stage (2 x 64 KB)
-// filled by direct global->LDS loads (no staging registers).  A 256 x 64
-// operand tile is stored as rows of eight 16-byte chunks; chunk c of row r
-// sits at slot c ^ ((r >> 1) & 7): the 16 lanes that one ds_read_b128 cycle
-// serves read 16 consecutive rows, and the swizzle gives every (row parity,
-// slot) pair once, i.e. all 64 banks.  Each stage lives in its own
-// __shared__ array so the compiler can tell the in-flight loads of one stage
-// from the reads of the other.
+//
+// Operand pipeline.  K advances in stages of 64.  Stages go to LDS with
+// buffer loads straight into LDS (no staging registers): A through a ring of
+// three 32 KB buffers, loaded two stages ahead, B through two, loaded one
+// stage ahead (5 x 32 KB = the whole 160 KB LDS).  A wave's eight loads of a
+// stage are spread through its MFMA stream (one after every four MFMAs)
+// instead of being issued in one burst after the barrier: all workgroups
+// bursting at once queue in L2 and roughly double the load latency.  Each
+// buffer is its own __shared__ array, so the compiler can tell the in-flight
+// loads of one buffer from the reads of another.  The buffer resources are
+// per tile with the tile's valid rows as their size: rows past M read as
+// zero (and only feed outputs that are never stored).
+//
+// A 256 x 64 operand tile is stored as rows of eight 16-byte chunks; chunk c
+// of row r sits at slot c ^ ((r >> 1) & 7): the 16 lanes that one
+// ds_read_b128 cycle serves read 16 consecutive rows, and the swizzle gives
+// every (row parity, slot) pair once, i.e. all 64 banks.
 //
 // Determinism: every output element is the same fixed sequence of MFMA
 // accumulations over k regardless of M, of the tile it sits in, and of the
@@ -22,7 +31,7 @@
 //
 // Workgroup -> tile order: the hardware deals workgroups to the 8 XCDs
 // round-robin; ids are remapped so each XCD walks a contiguous range of a
-// row-grouped tile order (8 row-tiles per group), which keeps the A and B
+// row-grouped tile order (4 row-tiles per group), which keeps the A and B
 // panels the co-resident workgroups of an XCD share in that XCD's L2.
 #include "epilogue.h"
 
@@ -36,8 +45,11 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int kThreads = 512;
-constexpr int kGroupM = 8;
+constexpr int kGroupM = 4;
 constexpr int kXcds = 8;
+constexpr int kLoadEvery = 4;  // MFMAs between two operand loads of a wave
+// s_waitcnt immediates (vmcnt in bits 3:0, expcnt and lgkmcnt left at their maxima)
+constexpr int kVmcnt0 = 0xF70, kVmcnt4 = 0xF74;
 
 __device__ inline int slot(int row, int chunk) { return row * 8 + (chunk ^ ((row >> 1) & 7)); }
 
@@ -58,31 +70,40 @@ __device__ inline bool map_tile(int bid, int nblocks, int ntm, int ntn, int& tm,
   return true;
 }
 
+// Raw buffer resource (gfx9 layout: stride 0, dword 3 = 0x00020000) over
+// `bytes` bytes at p; loads at offsets >= bytes return zero.
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+
 template <int KIND, int HD>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Bw, int M, int K, int ntm,
     int ntn, EpiArgs e) {
-  __shared__ u32x4 sA0[BM * 8], sB0[BN * 8], sA1[BM * 8], sB1[BN * 8];  // 4 x 32 KB
+  __shared__ u32x4 sA0[BM * 8], sA1[BM * 8], sA2[BM * 8];  // 3 x 32 KB
+  __shared__ u32x4 sB0[BN * 8], sB1[BN * 8];               // 2 x 32 KB
 
   int tm, tn;
   if (!map_tile(blockIdx.x, gridDim.x, ntm, ntn, tm, tn)) return;
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 2, wn = wave & 3;
 
-  // Direct global->LDS loads (16 B per lane): load i of wave w fills LDS rows
-  // (w*4 + i)*8 .. +8; lane l lands at row +l/8, slot l%8, so it fetches the
-  // logical chunk that the swizzle puts there.
-  const uint16_t* ga[4];
-  const uint16_t* gb[4];
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + (int64_t)m0 * K, min(M - m0, BM) * K * 2);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bw + (int64_t)n0 * K, BN * K * 2);
+  // Load i of wave w fills LDS rows (w*4 + i)*8 .. +8 of a stage; lane l lands
+  // at row +l/8, slot l%8 (the hardware writes lane l at base + 16 l), so it
+  // fetches the logical chunk the swizzle puts there.  The row is part of the
+  // lane offset (for the bounds check), the stage's k offset is scalar.
+  int voff[4];
 #pragma unroll
   for (int i = 0; i < 4; i++) {
     const int row = (wave * 4 + i) * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ ((row >> 1) & 7);
-    ga[i] = A + (int64_t)min(m0 + row, M - 1) * K + lc * 8;
-    gb[i] = Bw + (int64_t)(n0 + row) * K + lc * 8;
+    voff[i] = (row * K + lc * 8) * 2;
   }
 
   f32x4 acc[8][4];
@@ -95,15 +116,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   // 8 k-values of chunk (l >> 4) of the 32-wide k step.
   const int arow0 = wm * 128 + (lane & 15), brow0 = wn * 64 + (lane & 15), kq = lane >> 4;
 
-  auto load = [&](u32x4* sa, u32x4* sb, int k0) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int blk = (wave * 4 + i) * 64;
-      __builtin_amdgcn_global_load_lds((const void*)(ga[i] + k0), (lds_ptr_t)(sa + blk), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((const void*)(gb[i] + k0), (lds_ptr_t)(sb + blk), 16, 0, 0);
-    }
+  auto ldA = [&](u32x4* sa, int i, int k0) __attribute__((always_inline)) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(sa + (wave * 4 + i) * 64), 16, voff[i],
+                                             k0 * 2, 0, 0);
   };
-  auto compute = [&](const u32x4* sa, const u32x4* sb) __attribute__((always_inline)) {
+  auto ldB = [&](u32x4* sb, int i, int k0) __attribute__((always_inline)) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(sb + (wave * 4 + i) * 64), 16, voff[i],
+                                             k0 * 2, 0, 0);
+  };
+  // One stage from (sa, sb).  B of stage kb goes to nb and A of stage ka to na
+  // (negative: no load), one load after every kLoadEvery MFMAs.
+  auto compute = [&](const u32x4* sa, const u32x4* sb, u32x4* na, int ka, u32x4* nb, int kb)
+      __attribute__((always_inline)) {
+    int issued = 0, nm = 0;
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ks++) {
       const int ch = ks * 4 + kq;
@@ -115,29 +140,72 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
 #pragma unroll
       for (int i = 0; i < 8; i++)
 #pragma unroll
-        for (int j = 0; j < 4; j++)
+        for (int j = 0; j < 4; j++) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+          if (++nm % kLoadEvery == 0 && issued < 8) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (issued < 4) {
+              if (kb >= 0) ldB(nb, issued, kb);
+            } else {
+              if (ka >= 0) ldA(na, issued - 4, ka);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            issued++;
+          }
+        }
     }
   };
+  auto barrier = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
 
+  // Stage t reads A buffer t % 3 and B buffer t % 2.  During stage t a wave
+  // loads B(t+1) (into the B buffer stage t-1 used) and A(t+2) (into the A
+  // buffer of stage t-1), in that order; at the start of stage t its loads in
+  // flight are, oldest first, A(t), B(t), A(t+1), so vmcnt(4) leaves only
+  // A(t+1) outstanding.  The barrier then makes every wave's part of stage t
+  // visible, and ends every wave's reads of stage t-1.
+  auto full = [&](int t, const u32x4* ca, const u32x4* cb, u32x4* nb, u32x4* na)
+      __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(kVmcnt4);
+    barrier();
+    compute(ca, cb, na, (t + 2) * BK, nb, (t + 1) * BK);
+  };
   const int nk = K / BK;
-  load(sA0, sB0, 0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  int kt = 0;
-  for (; kt + 2 <= nk; kt += 2) {
-    load(sA1, sB1, (kt + 1) * BK);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(sA0, sB0);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (kt + 2 < nk) load(sA0, sB0, (kt + 2) * BK);
-    __builtin_amdgcn_sched_barrier(0);
-    compute(sA1, sB1);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+  auto tail = [&](int t, const u32x4* ca, const u32x4* cb, u32x4* nb, u32x4* na)
+      __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(kVmcnt0);
+    barrier();
+    compute(ca, cb, na, t + 2 < nk ? (t + 2) * BK : -1, nb, t + 1 < nk ? (t + 1) * BK : -1);
+  };
+#pragma unroll
+  for (int i = 0; i < 4; i++) ldA(sA0, i, 0);
+#pragma unroll
+  for (int i = 0; i < 4; i++) ldB(sB0, i, 0);
+  if (nk > 1) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) ldA(sA1, i, BK);
   }
-  if (kt < nk) compute(sA0, sB0);
+  // buffers repeat every 6 stages; the loop runs while all six steps and the
+  // loads they issue are in range, the rest (at most 7 stages) is predicated
+  int t = 0;
+  for (; t + 8 <= nk; t += 6) {
+    full(t + 0, sA0, sB0, sB1, sA2);
+    full(t + 1, sA1, sB1, sB0, sA0);
+    full(t + 2, sA2, sB0, sB1, sA1);
+    full(t + 3, sA0, sB1, sB0, sA2);
+    full(t + 4, sA1, sB0, sB1, sA0);
+    full(t + 5, sA2, sB1, sB0, sA1);
+  }
+  if (t + 0 < nk) tail(t + 0, sA0, sB0, sB1, sA2);
+  if (t + 1 < nk) tail(t + 1, sA1, sB1, sB0, sA0);
+  if (t + 2 < nk) tail(t + 2, sA2, sB0, sB1, sA1);
+  if (t + 3 < nk) tail(t + 3, sA0, sB1, sB0, sA2);
+  if (t + 4 < nk) tail(t + 4, sA1, sB0, sB1, sA0);
+  if (t + 5 < nk) tail(t + 5, sA2, sB1, sB0, sA1);
+  if (t + 6 < nk) tail(t + 6, sA0, sB0, sB1, sA2);
 
   // Epilogue.  16 x 16 block layout: lane holds column (lane & 15) and rows
   // 4 (lane >> 4) + r, r = 0..3.  Blocks j and j + 2 give the column pair
