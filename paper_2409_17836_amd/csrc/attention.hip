@@ -15,9 +15,10 @@
 // cross-lane exchange (lane ^ 32) instead of a 32-lane reduction.  The K rows
 // are fed to the MFMA in a permuted order so that the score registers are,
 // without any shuffle, the B operand of O^T += V^T P^T.  Softmax statistics
-// are float32 in base 2 (the 1/sqrt(hd) scale folded into the exponent); the
-// output is rescaled only when a query's running maximum moves; P is rounded
-// to bf16 for the second product; O is normalised at the end.
+// are float32 in base 2 (the 1/sqrt(hd) scale folded into the exponent); a
+// query's reference maximum moves, and O is rescaled, only when a score
+// exceeds it by more than 2^8 in probability; P is rounded to bf16 for the
+// second product; O is normalised at the end.
 //
 // Determinism / prefix invariance: a query's key tiles are processed in a
 // fixed order that depends only on the query's 128-query block; masked keys
@@ -60,6 +61,8 @@ __device__ inline uint32_t pack2(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+constexpr float kLazy = 8.0f;  // log2 headroom of the lazily moved softmax reference
+
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
@@ -97,6 +100,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
 #pragma unroll
   for (int i = 0; i < NOB; i++) oacc[i] = f32x16{};
   float m_i = -INFINITY, l_i = 0.f;
+  const float lazy = kLazy / sl2;
 
   // MFMA row rho = 8a + 4g + c (a = rho/8, g = (rho/4)&1, c = rho&3) takes key
   // 16 (a/2) + 8 g + 4 (a&1) + c of its 32-key block.
@@ -168,26 +172,30 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
         }
       }
 #pragma unroll
-      for (int r = 0; r < 16; r++) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mnew = fmaxf(m_i, mx);
-      const float nms = -mnew * sl2;
-      float ls = 0.f;
+      for (int r = 0; r < 16; r++) mx = fmaxf(fmaxf(mx, s0[r]), s1[r]);  // v_max3
+      // Lazy rescaling: a query's reference point m_i moves only when one of
+      // its scores exceeds it by more than kLazy/sl2 (probabilities stay below
+      // 2^kLazy), and then to the maximum over both lane halves; both halves
+      // hold the same m_i.  A wave-wide ballot finds out whether any lane needs
+      // this; only then are the halves' maxima exchanged.  Either way a query
+      // rescales exactly when its own maximum passes the threshold.
+      if (__ballot(mx > m_i + lazy)) {
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        if (mx > m_i + lazy) {
+          const float alpha = __builtin_amdgcn_exp2f((m_i - mx) * sl2);
+          l_i *= alpha;
+#pragma unroll
+          for (int i = 0; i < NOB; i++) oacc[i] *= alpha;
+          m_i = mx;
+        }
+      }
+      const float nms = -m_i * sl2;
 #pragma unroll
       for (int r = 0; r < 16; r++) {
         s0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nms));
         s1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nms));
-        ls += s0[r] + s1[r];
+        l_i += s0[r] + s1[r];  // this half's keys; the halves are added at the end
       }
-      ls += __shfl_xor(ls, 32, 64);
-      if (mnew != m_i) {  // running max moved: rescale (skipped when the factor is exactly 1)
-        const float alpha = __builtin_amdgcn_exp2f((m_i - mnew) * sl2);
-        l_i *= alpha;
-#pragma unroll
-        for (int i = 0; i < NOB; i++) oacc[i] *= alpha;
-      }
-      l_i += ls;
-      m_i = mnew;
 
       bf16x8 pf[4];
 #pragma unroll
@@ -221,6 +229,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   }
   if (t < ntiles) tile(t, sK0, sV0, sK1, sV1);
 
+  l_i += __shfl_xor(l_i, 32, 64);
   if (myq < W) {
     const float inv = 1.0f / l_i;
     uint16_t* orow = o + ((int64_t)b * W + myq) * (int64_t)(Hq * HD) + h * HD;
