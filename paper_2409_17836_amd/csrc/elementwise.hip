@@ -60,7 +60,8 @@ __global__ void embed_kernel(const int32_t* __restrict__ tokens, int B, int W, i
 }
 
 // ------------------------------------------------------------------- norms
-// One wave per row; lane l keeps elements l, l+64, ... in registers.
+// One wave per row; lane l keeps elements l, l+64, ... in registers (general
+// case: any d that is a multiple of 64, float32 or bf16 output).
 template <int MAXV>
 __global__ void norm_kernel(const float* __restrict__ h, int M, int d, const void* __restrict__ g,
                             const void* __restrict__ b, int layernorm, float eps, int dtype,
@@ -101,6 +102,56 @@ __global__ void norm_kernel(const float* __restrict__ h, int M, int d, const voi
       ((__bf16*)y)[row * d + c] = (__bf16)t;
     else
       ((float*)y)[row * d + c] = t;
+  }
+}
+
+// bf16 output, d = 256 * NV4: lane l keeps the float4 chunks l, l+64, ... of
+// the row (1 KB per wave load), writes four bf16 per store and reads the
+// gains (and biases) four at a time.
+template <int NV4>
+__global__ void norm_bf16x4_kernel(const float* __restrict__ h, int M, const uint16_t* __restrict__ g,
+                                   const uint16_t* __restrict__ b, int layernorm, float eps,
+                                   __bf16* __restrict__ y) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  constexpr int d = NV4 * 4 * kWave;
+  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (row >= M) return;
+  const float4* x = reinterpret_cast<const float4*>(h + row * d);
+  float4 v[NV4];
+#pragma unroll
+  for (int i = 0; i < NV4; i++) v[i] = x[i * kWave + lane];
+  float mean = 0.f;
+  if (layernorm) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV4; i++) s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    mean = wave_sum(s) / (float)d;
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV4; i++) {
+    const float a0 = v[i].x - mean, a1 = v[i].y - mean, a2 = v[i].z - mean, a3 = v[i].w - mean;
+    ss += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+  }
+  const float r = 1.0f / sqrtf(wave_sum(ss) / (float)d + eps);
+  bf16x4* out = reinterpret_cast<bf16x4*>(y + row * d);
+#pragma unroll
+  for (int i = 0; i < NV4; i++) {
+    const int c4 = i * kWave + lane;
+    const uint2 gg = reinterpret_cast<const uint2*>(g)[c4];
+    float t0 = (v[i].x - mean) * r * bf16_to_f32(gg.x & 0xFFFF);
+    float t1 = (v[i].y - mean) * r * bf16_to_f32(gg.x >> 16);
+    float t2 = (v[i].z - mean) * r * bf16_to_f32(gg.y & 0xFFFF);
+    float t3 = (v[i].w - mean) * r * bf16_to_f32(gg.y >> 16);
+    if (layernorm) {
+      const uint2 bb = reinterpret_cast<const uint2*>(b)[c4];
+      t0 += bf16_to_f32(bb.x & 0xFFFF);
+      t1 += bf16_to_f32(bb.x >> 16);
+      t2 += bf16_to_f32(bb.y & 0xFFFF);
+      t3 += bf16_to_f32(bb.y >> 16);
+    }
+    out[c4] = bf16x4{(__bf16)t0, (__bf16)t1, (__bf16)t2, (__bf16)t3};
   }
 }
 
@@ -206,6 +257,30 @@ hipError_t launch_norm(const float* h, int M, int d, const void* gain, const voi
                        int layernorm, float eps, int dtype, void* y, hipStream_t s) {
   const dim3 grid((unsigned)((M + 3) / 4));
   if (d % kWave != 0 || d > 8192) return hipErrorInvalidValue;
+  if (dtype == LMGC_DTYPE_BF16 && d % 256 == 0) {
+    const uint16_t* g16 = (const uint16_t*)gain;
+    const uint16_t* b16 = (const uint16_t*)bias;
+    __bf16* yb = (__bf16*)y;
+    switch (d / 256) {
+      case 2:
+        hipLaunchKernelGGL(norm_bf16x4_kernel<2>, grid, dim3(256), 0, s, h, M, g16, b16, layernorm, eps, yb);
+        return hipGetLastError();
+      case 3:
+        hipLaunchKernelGGL(norm_bf16x4_kernel<3>, grid, dim3(256), 0, s, h, M, g16, b16, layernorm, eps, yb);
+        return hipGetLastError();
+      case 4:
+        hipLaunchKernelGGL(norm_bf16x4_kernel<4>, grid, dim3(256), 0, s, h, M, g16, b16, layernorm, eps, yb);
+        return hipGetLastError();
+      case 8:
+        hipLaunchKernelGGL(norm_bf16x4_kernel<8>, grid, dim3(256), 0, s, h, M, g16, b16, layernorm, eps, yb);
+        return hipGetLastError();
+      case 16:
+        hipLaunchKernelGGL(norm_bf16x4_kernel<16>, grid, dim3(256), 0, s, h, M, g16, b16, layernorm, eps, yb);
+        return hipGetLastError();
+      default:
+        break;  // the general kernel below
+    }
+  }
   if (d <= 1024)
     hipLaunchKernelGGL(norm_kernel<16>, grid, dim3(256), 0, s, h, M, d, gain, bias, layernorm,
                        eps, dtype, y);
