@@ -6,10 +6,12 @@
 // bf16 kernel (CDNA4 matrix cores).  A workgroup of four 64-wide waves owns
 // 128 queries of one (window, head); each wave 32 queries.  Tiles of 64 keys
 // of K [key][dim] and of V^T [dim][key] (the QKV projection writes V
-// transposed) go to LDS with direct global->LDS loads into two buffers: the
-// next tile streams in while the current one is used, with one barrier per
-// tile; each buffer is its own __shared__ array so the compiler can tell the
-// in-flight loads of one buffer from the reads of the other.  The wave
+// transposed) go to LDS with direct global->LDS loads into two buffers each,
+// K one tile ahead of V, with one barrier per tile; each buffer is its own
+// __shared__ array so the compiler can tell the in-flight loads of one buffer
+// from the reads of the other.  Each wave issues the S MFMAs of the next tile
+// before the softmax of the current one, so the exponentials overlap matrix
+// work.  The wave
 // computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so each lane holds one
 // query's scores in its own registers: the row max / row sum need one
 // cross-lane exchange (lane ^ 32) instead of a 32-lane reduction.  The K rows
@@ -18,7 +20,8 @@
 // are float32 in base 2 (the 1/sqrt(hd) scale folded into the exponent); a
 // query's reference maximum moves, and O is rescaled, only when a score
 // exceeds it by more than 2^8 in probability; P is rounded to bf16 for the
-// second product; O is normalised at the end.
+// second product and the row sums are taken over the rounded P (v_dot2 with
+// ones); O is normalised at the end.
 //
 // Determinism / prefix invariance: a query's key tiles are processed in a
 // fixed order that depends only on the query's 128-query block; masked keys
@@ -50,6 +53,12 @@ template <int HD>
 __device__ inline int kswz(int key) { return HD == 128 ? (key & 15) : ((key >> 1) & 7); }
 __device__ inline int vswz(int d) { return (d >> 1) & 7; }
 
+// Raw buffer resource (gfx9 layout: stride 0, dword 3 = 0x00020000) over
+// `bytes` bytes at p.
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+
 // key held by score register r of a lane in half h (see the S^T layout).
 __device__ inline int key_of_reg(int r, int h) { return r < 8 ? 8 * h + r : 16 + 8 * h + (r - 8); }
 
@@ -80,7 +89,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   const int qb = nqb - 1 - (int)blockIdx.x;  // longest blocks first
   const int h = blockIdx.y, b = blockIdx.z;
   const int kvh = h * Hkv / Hq;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, c32 = lane & 31;
   const int q0 = qb * BQ + wave * 32;
   const int myq = q0 + c32;
@@ -136,98 +146,168 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
                                        (lds_ptr_t)(sVb + (wave * NVD + i) * 64), 16, 0, 0);
     }
   };
+  // Full tiles (k0 + BKV <= W) load through buffer resources over this
+  // (window, kv head)'s K and V^T, with lane offsets fixed for the whole loop
+  // and the tile's offset in a scalar; a ragged last tile takes the clamped
+  // loads above.
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(Kp, W * HD * 2);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(Vp, HD * W * 2);
+  // (fixed array sizes: with sizes that depend on HD the host compilation
+  // pass silently dropped this kernel's launch stub)
+  static_assert(NKL <= 4 && NVD <= 4, "offset arrays hold four loads");
+  int kvo[4], vvo[4];
+#pragma unroll
+  for (int i = 0; i < NKL; i++) {
+    const int key = (wave * NKL + i) * KROWS + lane / KCH;
+    kvo[i] = (key * HD + ((lane % KCH) ^ kswz<HD>(key)) * 8) * 2;
+  }
+#pragma unroll
+  for (int i = 0; i < NVD; i++) {
+    const int d = (wave * NVD + i) * 8 + lane / 8;
+    vvo[i] = (d * W + ((lane % 8) ^ vswz(d)) * 8) * 2;
+  }
+  auto kload_full = [&](u32x4* sKb, int k0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NKL; i++)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_ptr_t)(sKb + (wave * NKL + i) * 64), 16,
+                                               kvo[i], k0 * HD * 2, 0, 0);
+  };
+  auto vtload_full = [&](u32x4* sVb, int k0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < NVD; i++)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_ptr_t)(sVb + (wave * NVD + i) * 64), 16,
+                                               vvo[i], k0 * 2, 0, 0);
+  };
+  auto kload_any = [&](u32x4* sKb, int k0) __attribute__((always_inline)) {
+    if (k0 + BKV <= W) kload_full(sKb, k0);
+    else kload(sKb, k0);
+  };
+  auto vtload_any = [&](u32x4* sVb, int k0) __attribute__((always_inline)) {
+    if (k0 + BKV <= W) vtload_full(sVb, k0);
+    else vtload(sVb, k0);
+  };
   const int kend = min(W, qb * BQ + BQ);
   const int ntiles = (kend + BKV - 1) / BKV;
-  auto tile = [&](int t, const u32x4* sKc, const u32x4* sVc, u32x4* sKn, u32x4* sVn)
+  // S^T of key tile t (64 keys, two 32-key blocks) from the K tile in sKc.
+  auto qk = [&](const u32x4* sKc, f32x16& s0, f32x16& s1) __attribute__((always_inline)) {
+    s0 = f32x16{};
+    s1 = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < NKS; ks++) {
+      const int ch = 2 * ks + half;
+      const int key0 = kperm, key1 = 32 + kperm;
+      const bf16x8 ka = as_bf16x8(sKc[key0 * KCH + (ch ^ kswz<HD>(key0))]);
+      const bf16x8 kb = as_bf16x8(sKc[key1 * KCH + (ch ^ kswz<HD>(key1))]);
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[ks], s1, 0, 0, 0);
+    }
+  };
+  // softmax of tile t's scores (masking, lazy reference, exponentials, row
+  // sums) and O^T += V^T P^T with the V^T tile in sVc
+  auto softmax_pv = [&](int t, f32x16& s0, f32x16& s1, const u32x4* sVc)
       __attribute__((always_inline)) {
     const int k0 = t * BKV;
-    // tile t is in (sKc, sVc); every wave is done with tile t-1, whose
-    // buffers (sKn, sVn) are refilled with tile t+1 during this tile's math
-    __syncthreads();
-    if (t + 1 < ntiles) {
-      kload(sKn, k0 + BKV);
-      vtload(sVn, k0 + BKV);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    if (k0 <= q0 + 31) {  // else the tile lies entirely after this wave's queries
-      f32x16 s0 = f32x16{}, s1 = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < NKS; ks++) {
-        const int ch = 2 * ks + half;
-        const int key0 = kperm, key1 = 32 + kperm;
-        const bf16x8 ka = as_bf16x8(sKc[key0 * KCH + (ch ^ kswz<HD>(key0))]);
-        const bf16x8 kb = as_bf16x8(sKc[key1 * KCH + (ch ^ kswz<HD>(key1))]);
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf[ks], s1, 0, 0, 0);
-      }
-      // scores stay unscaled: p = 2^(s*sl2 - m*sl2) with m the running raw max
-      float mx = -INFINITY;
-      const bool diag = k0 + BKV - 1 > q0;  // some key of the tile may lie after a query
-      if (diag) {
-#pragma unroll
-        for (int r = 0; r < 16; r++) {
-          const int key = k0 + key_of_reg(r, half);
-          if (key > myq) s0[r] = -INFINITY;
-          if (key + 32 > myq) s1[r] = -INFINITY;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < 16; r++) mx = fmaxf(fmaxf(mx, s0[r]), s1[r]);  // v_max3
-      // Lazy rescaling: a query's reference point m_i moves only when one of
-      // its scores exceeds it by more than kLazy/sl2 (probabilities stay below
-      // 2^kLazy), and then to the maximum over both lane halves; both halves
-      // hold the same m_i.  A wave-wide ballot finds out whether any lane needs
-      // this; only then are the halves' maxima exchanged.  Either way a query
-      // rescales exactly when its own maximum passes the threshold.
-      if (__ballot(mx > m_i + lazy)) {
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        if (mx > m_i + lazy) {
-          const float alpha = __builtin_amdgcn_exp2f((m_i - mx) * sl2);
-          l_i *= alpha;
-#pragma unroll
-          for (int i = 0; i < NOB; i++) oacc[i] *= alpha;
-          m_i = mx;
-        }
-      }
-      const float nms = -m_i * sl2;
+    // scores stay unscaled: p = 2^(s*sl2 - m*sl2) with m the reference maximum
+    float mx = -INFINITY;
+    const bool diag = k0 + BKV - 1 > q0;  // some key of the tile may lie after a query
+    if (diag) {
 #pragma unroll
       for (int r = 0; r < 16; r++) {
-        s0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nms));
-        s1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nms));
-        l_i += s0[r] + s1[r];  // this half's keys; the halves are added at the end
+        const int key = k0 + key_of_reg(r, half);
+        if (key > myq) s0[r] = -INFINITY;
+        if (key + 32 > myq) s1[r] = -INFINITY;
       }
-
-      bf16x8 pf[4];
+    }
 #pragma unroll
-      for (int kk = 0; kk < 4; kk++) {
-        const f32x16& sv = (kk < 2) ? s0 : s1;
-        const int r0 = (kk & 1) * 8;
-        const u32x4 u = {pack2(sv[r0 + 0], sv[r0 + 1]), pack2(sv[r0 + 2], sv[r0 + 3]),
-                         pack2(sv[r0 + 4], sv[r0 + 5]), pack2(sv[r0 + 6], sv[r0 + 7])};
-        pf[kk] = as_bf16x8(u);
+    for (int r = 0; r < 16; r++) mx = fmaxf(fmaxf(mx, s0[r]), s1[r]);  // v_max3
+    // Lazy rescaling: a query's reference point m_i moves only when one of
+    // its scores exceeds it by more than kLazy/sl2 (probabilities stay below
+    // 2^kLazy), and then to the maximum over both lane halves; both halves
+    // hold the same m_i.  A wave-wide ballot finds out whether any lane needs
+    // this; only then are the halves' maxima exchanged.  Either way a query
+    // rescales exactly when its own maximum passes the threshold.
+    if (__ballot(mx > m_i + lazy)) {
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      if (mx > m_i + lazy) {
+        const float alpha = __builtin_amdgcn_exp2f((m_i - mx) * sl2);
+        l_i *= alpha;
+#pragma unroll
+        for (int i = 0; i < NOB; i++) oacc[i] *= alpha;
+        m_i = mx;
       }
+    }
+    const float nms = -m_i * sl2;
+#pragma unroll
+    for (int r = 0; r < 16; r++) {
+      s0[r] = __builtin_amdgcn_exp2f(fmaf(s0[r], sl2, nms));
+      s1[r] = __builtin_amdgcn_exp2f(fmaf(s1[r], sl2, nms));
+    }
+    // P rounded to bf16; the row sum is taken over these rounded values (the
+    // ones P V uses), two per v_dot2 against (1, 1), over this half's keys
+    // (the halves are added at the end)
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    bf16x8 pf[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; kk++) {
+      const f32x16& sv = (kk < 2) ? s0 : s1;
+      const int r0 = (kk & 1) * 8;
+      // (the dot2 operands are the packed words themselves: reading them back
+      // out of the u32x4 below made this compiler feed element 0 to all four)
+      const uint32_t w0 = pack2(sv[r0 + 0], sv[r0 + 1]), w1 = pack2(sv[r0 + 2], sv[r0 + 3]);
+      const uint32_t w2 = pack2(sv[r0 + 4], sv[r0 + 5]), w3 = pack2(sv[r0 + 6], sv[r0 + 7]);
+      l_i = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), ones, l_i, false);
+      l_i = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), ones, l_i, false);
+      l_i = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), ones, l_i, false);
+      l_i = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w3), ones, l_i, false);
+      const u32x4 u = {w0, w1, w2, w3};
+      pf[kk] = as_bf16x8(u);
+    }
+    // k-step outer: the NOB accumulations of a step are independent chains
+#pragma unroll
+    for (int kk = 0; kk < 4; kk++) {
+      bf16x8 va[NOB];
 #pragma unroll
       for (int i = 0; i < NOB; i++) {
         const int d = i * 32 + c32;
-#pragma unroll
-        for (int kk = 0; kk < 4; kk++) {
-          const bf16x8 va = as_bf16x8(sVc[d * 8 + ((2 * kk + half) ^ vswz(d))]);
-          oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[kk], oacc[i], 0, 0, 0);
-        }
+        va[i] = as_bf16x8(sVc[d * 8 + ((2 * kk + half) ^ vswz(d))]);
       }
+#pragma unroll
+      for (int i = 0; i < NOB; i++)
+        oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i], pf[kk], oacc[i], 0, 0, 0);
     }
+  };
+  // Software pipeline, one step per key tile t: K runs one tile ahead of V.
+  // At step t, K(t+1) and V(t) are in LDS; the wave issues the S MFMAs of tile
+  // t+1 first, so the matrix cores work on them while it does the softmax of
+  // tile t (whose scores it computed in the previous step), then the P V
+  // MFMAs of tile t.  Meanwhile K(t+2) and V(t+1) stream into the buffers of
+  // K(t) and V(t-1), which every wave finished with before the step's barrier.
+  // A tile lying entirely after the wave's 32 queries is skipped.
+  const int tlast = min(ntiles - 1, (q0 + 31) / BKV);  // last tile this wave needs
+  f32x16 sa0, sa1, sb0, sb1;                          // scores of two tiles in flight
+  auto step = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1, const u32x4* sKn,
+                  const u32x4* sVc, u32x4* sKf, u32x4* sVf) __attribute__((always_inline)) {
+    __syncthreads();
+    if (t + 2 < ntiles) kload_any(sKf, (t + 2) * BKV);
+    if (t + 1 < ntiles) vtload_any(sVf, (t + 1) * BKV);
+    __builtin_amdgcn_sched_barrier(0);
+    if (t + 1 <= tlast) qk(sKn, n0, n1);
+    if (t <= tlast) softmax_pv(t, c0, c1, sVc);
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   };
-  kload(sK0, 0);
-  vtload(sV0, 0);
+  kload_any(sK0, 0);
+  vtload_any(sV0, 0);
+  if (ntiles > 1) kload_any(sK1, BKV);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  qk(sK0, sa0, sa1);
   int t = 0;
   for (; t + 2 <= ntiles; t += 2) {
-    tile(t, sK0, sV0, sK1, sV1);
-    tile(t + 1, sK1, sV1, sK0, sV0);
+    step(t, sa0, sa1, sb0, sb1, sK1, sV0, sK0, sV1);
+    step(t + 1, sb0, sb1, sa0, sa1, sK0, sV1, sK1, sV0);
   }
-  if (t < ntiles) tile(t, sK0, sV0, sK1, sV1);
+  if (t < ntiles) step(t, sa0, sa1, sb0, sb1, sK1, sV0, sK0, sV1);
 
   l_i += __shfl_xor(l_i, 32, 64);
   if (myq < W) {
