@@ -184,6 +184,22 @@ int lmgc_probs(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t 
                const lmgc_serial_params* p, uint32_t total, uint32_t* d_cdf, float* d_logp,
                void* d_ws, size_t ws_bytes, void* stream);
 
+/*
+ * The same tables as lmgc_probs, computed one position at a time the way the
+ * decoder computes them (Sec. 4, "Compression": decompression starts from
+ * BOS and feeds each decoded token back): every step runs the LM on one row
+ * per window, reading the K and V of earlier positions from a per-layer
+ * cache.  Each row's arithmetic is the one lmgc_probs does for that row, so
+ * d_cdf (and d_logp) equal lmgc_probs' outputs bit for bit; tests use this
+ * to check the decoder's path without arithmetic coding.  d_tokens [B, W]
+ * device, B <= 16, other arguments and layouts as lmgc_probs.  Workspace:
+ * lmgc_step_workspace(m, B, W) bytes (0 if B > 16).  GPU, async.
+ */
+size_t lmgc_step_workspace(const lmgc_model* m, int32_t B, int32_t W);
+int lmgc_probs_stepwise(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t W,
+                        const lmgc_serial_params* p, uint32_t total, uint32_t* d_cdf,
+                        float* d_logp, void* d_ws, size_t ws_bytes, void* stream);
+
 /* ---------------------------------------------------------------- coding */
 /*
  * Arithmetic coding (Sec. 3): a Witten-Neal-Cleary binary arithmetic coder
@@ -231,7 +247,9 @@ int lmgc_decode_symbol(lmgc_decoder* st, const uint32_t* cdf_row, int32_t nsym,
 /* Upper bound of the container size for n_values values. */
 size_t lmgc_container_bound(int64_t n_values, const lmgc_serial_params* p);
 
-/* Device workspace bytes lmgc_compress / lmgc_decode need. */
+/* Device workspace bytes lmgc_compress / lmgc_decode need (the larger of
+ * the two: compression holds one batch's activations, decoding the K/V
+ * cache of up to min(batch, 16) windows). */
 size_t lmgc_codec_workspace(const lmgc_model* m, int64_t n_values, const lmgc_serial_params* p,
                             int32_t batch);
 
@@ -251,8 +269,11 @@ int lmgc_compress(const lmgc_model* m, const void* d_values, int64_t n_values,
 
 /*
  * Decompress a whole-vector container into values_out (host, n_values *
- * bytes_per_value bytes).  Decodes window batches token by token from BOS,
- * re-running lmgc_probs on the decoded prefix at every step.  expect_tag
+ * bytes_per_value bytes).  Decodes groups of min(batch, 16) windows token by
+ * token from BOS: each step computes the next position's tables of the
+ * group through the K/V cache (as lmgc_probs_stepwise, bit for bit the
+ * encoder's tables), the host decodes one symbol per window and its token
+ * is the next step's input.  expect_tag
  * must equal the header's model tag.  Errors: ECORRUPT (bad container,
  * escape symbol, malformed stream, tag mismatch), ESIZE, EDEVICE.
  */

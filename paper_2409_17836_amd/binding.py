@@ -79,6 +79,9 @@ def lib():
         "lmgc_model_destroy": (None, [vp]),
         "lmgc_probs_workspace": (sz, [vp, i32, i32]),
         "lmgc_probs": (ctypes.c_int, [vp, vp, i32, i32, P(SerialParams), u32, vp, vp, vp, sz, vp]),
+        "lmgc_step_workspace": (sz, [vp, i32, i32]),
+        "lmgc_probs_stepwise": (ctypes.c_int, [vp, vp, i32, i32, P(SerialParams), u32, vp, vp, vp, sz,
+                                               vp]),
         "lmgc_encode_bound": (sz, [i32, i32]),
         "lmgc_encode": (ctypes.c_int, [vp, i32, vp, vp, i32, i32, vp, sz, vp, P(sz), i32]),
         "lmgc_decode_init": (ctypes.c_int, [P(DecoderState), vp, u64]),
@@ -233,6 +236,9 @@ class Model:
     def probs_workspace(self, B: int, W: int) -> int:
         return int(lib().lmgc_probs_workspace(self.handle, B, W))
 
+    def step_workspace(self, B: int, W: int) -> int:
+        return int(lib().lmgc_step_workspace(self.handle, B, W))
+
     def codec_workspace(self, n_values: int, sp: SerialParams, batch: int) -> int:
         return int(lib().lmgc_codec_workspace(self.handle, n_values, ctypes.byref(sp), batch))
 
@@ -260,6 +266,22 @@ def probs(model: Model, tokens, sp: SerialParams, total: int = 1 << 16, want_log
         logp = torch.empty((B, W, NALPHA), dtype=torch.float32, device=tokens.device)
     _check(lib().lmgc_probs(model.handle, _ptr(tokens), B, W, ctypes.byref(sp), total, _ptr(cdf),
                             _ptr(logp), _ptr(ws), ws.numel(), _stream(stream)))
+    return cdf, logp
+
+
+def probs_stepwise(model: Model, tokens, sp: SerialParams, total: int = 1 << 16,
+                   want_logp: bool = True, ws=None, stream=None):
+    """lmgc_probs_stepwise: the same outputs as probs(), computed position by
+    position through the K/V cache (the decoder's path); B <= 16."""
+    import torch
+    B, W = tokens.shape
+    assert tokens.dtype == torch.int32 and tokens.is_contiguous()
+    if ws is None:
+        ws = workspace(model.step_workspace(B, W), tokens.device)
+    cdf = torch.empty((B, W, NSYM + 1), dtype=torch.int32, device=tokens.device)
+    logp = torch.empty((B, W, NALPHA), dtype=torch.float32, device=tokens.device) if want_logp else None
+    _check(lib().lmgc_probs_stepwise(model.handle, _ptr(tokens), B, W, ctypes.byref(sp), total,
+                                     _ptr(cdf), _ptr(logp), _ptr(ws), ws.numel(), _stream(stream)))
     return cdf, logp
 
 

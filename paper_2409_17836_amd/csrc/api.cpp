@@ -391,6 +391,137 @@ static ProbsWs carve(const lmgc_model* m, int B, int W, char* base) {
 }
 
 // ---------------------------------------------------------------- forward
+// ---------------------------------------------------------------- forward
+// Activation buffers of one forward pass.  kc[l] / vc[l]: layer l's K and V
+// (V^T for bf16 models) in [B, Hkv, W, hd] ([B, Hkv, hd, W]) layout; a batch
+// of whole windows may point every layer at one buffer, a decoding step
+// keeps one per layer (the cache).
+struct FwdBufs {
+  float* h;
+  void *a, *q, *o, *ff;
+  float* logits;
+  void* const* kc;
+  void* const* vc;
+};
+
+// The decoder over B windows of W tokens.  dpos < 0: all W positions of each
+// window (rows b*W + j; tok is [B, W]).  dpos >= 0: one decoding step, the
+// row of position dpos of each window (rows b; tok[b] is the token at
+// dpos - 1; layers read K and V of earlier positions from the cache and add
+// their own).  Every kernel computes a row exactly as in the full pass, so
+// the step's tables equal the full pass's row dpos bit for bit.
+static int forward(const lmgc_model* m, const int32_t* tok, int B, int W, int dpos, const lmgc_serial_params* p,
+                   uint32_t total, const FwdBufs& f, uint32_t* cdf, float* logp, hipStream_t s) {
+  const lmgc_model_config& c = m->cfg;
+  const bool step = dpos >= 0;
+  const int M = step ? B : B * W, d = c.d_model, hd = m->hd, F = c.d_ff;
+  const bool bf = c.dtype == LMGC_DTYPE_BF16;
+  const bool llama = c.arch == LMGC_ARCH_LLAMA;
+  auto gemm = [&](const void* A, const void* Bw, int Npad, int K, EpiArgs e) {
+    e.step = step ? 1 : 0;
+    e.dpos = step ? dpos : 0;
+    if (!bf) return launch_gemm_f32((const float*)A, (const float*)Bw, M, Npad, K, e, s);
+    return step ? launch_gemm_bf16_rows((const uint16_t*)A, (const uint16_t*)Bw, M, Npad, K, e, s)
+                : launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)Bw, M, Npad, K, e, s);
+  };
+  {
+    ScopedTimer t(LMGC_K_EMBED, s);
+    HIP_OK(launch_embed(tok, B, W, p->bos_id, m->tok_emb, m->pos_emb, d, c.vocab, c.dtype, dpos, f.h, s));
+  }
+  for (int l = 0; l < c.n_layers; l++) {
+    const Layer& L = m->layers[l];
+    {
+      ScopedTimer t(LMGC_K_NORM, s);
+      HIP_OK(launch_norm(f.h, M, d, L.n1, L.n1b, !llama, c.norm_eps, c.dtype, f.a, s));
+    }
+    {
+      ScopedTimer t(LMGC_K_GEMM_QKV, s);
+      EpiArgs e = {};
+      e.kind = llama ? EPI_QKV_ROPE : EPI_QKV_BIAS;
+      e.M = M;
+      e.N = m->n_qkv;
+      e.bias = L.bqkv;
+      e.q = f.q;
+      e.k = f.kc[l];
+      e.v = f.vc[l];
+      e.W = W;
+      e.Hq = c.n_heads;
+      e.Hkv = c.n_kv_heads;
+      e.hd = hd;
+      e.rope = m->rope;
+      HIP_OK(gemm(f.a, L.wqkv, m->n_qkv_pad, d, e));
+    }
+    {
+      ScopedTimer t(LMGC_K_ATTN, s);
+      if (bf)
+        HIP_OK(launch_attention_bf16((const uint16_t*)f.q, (const uint16_t*)f.kc[l], (const uint16_t*)f.vc[l],
+                                     (uint16_t*)f.o, B, c.n_heads, c.n_kv_heads, W, hd, dpos, s));
+      else
+        HIP_OK(launch_attention_f32((const float*)f.q, (const float*)f.kc[l], (const float*)f.vc[l], (float*)f.o,
+                                    B, c.n_heads, c.n_kv_heads, W, hd, dpos, s));
+    }
+    {
+      ScopedTimer t(LMGC_K_GEMM_O, s);
+      EpiArgs e = {};
+      e.kind = EPI_RESID;
+      e.M = M;
+      e.N = d;
+      e.c = f.h;
+      e.ldc = d;
+      e.bias = L.bo;
+      HIP_OK(gemm(f.o, L.wo, m->d_pad, c.n_heads * hd, e));
+    }
+    {
+      ScopedTimer t(LMGC_K_NORM, s);
+      HIP_OK(launch_norm(f.h, M, d, L.n2, L.n2b, !llama, c.norm_eps, c.dtype, f.a, s));
+    }
+    {
+      ScopedTimer t(LMGC_K_GEMM_UP, s);
+      EpiArgs e = {};
+      e.kind = llama ? EPI_SWIGLU : EPI_BIAS_GELU;
+      e.M = M;
+      e.N = m->n_up;
+      e.bias = L.bup;
+      e.out = f.ff;
+      e.ld_out = F;
+      HIP_OK(gemm(f.a, L.wup, m->n_up_pad, d, e));
+    }
+    {
+      ScopedTimer t(LMGC_K_GEMM_DOWN, s);
+      EpiArgs e = {};
+      e.kind = EPI_RESID;
+      e.M = M;
+      e.N = d;
+      e.c = f.h;
+      e.ldc = d;
+      e.bias = L.bdown;
+      HIP_OK(gemm(f.ff, L.wdown, m->d_pad, F, e));
+    }
+  }
+  {
+    ScopedTimer t(LMGC_K_NORM, s);
+    HIP_OK(launch_norm(f.h, M, d, m->final_g, m->final_b, !llama, c.norm_eps, c.dtype, f.a, s));
+  }
+  {
+    ScopedTimer t(LMGC_K_GEMM_HEAD, s);
+    EpiArgs e = {};
+    e.kind = EPI_STORE_F32;
+    e.M = M;
+    e.N = c.vocab;
+    e.c = f.logits;
+    e.ldc = m->v_pad;
+    HIP_OK(gemm(f.a, m->head, m->v_pad, d, e));
+  }
+  {
+    ScopedTimer t(LMGC_K_LSE_CDF, s);
+    int32_t ids[LMGC_NALPHA];
+    for (int i = 0; i < 16; i++) ids[i] = p->hex_ids[i];
+    ids[16] = p->sep_id;
+    HIP_OK(launch_lse_cdf(f.logits, M, m->v_pad, c.vocab, ids, total, cdf, logp, s));
+  }
+  return LMGC_OK;
+}
+
 static int run_probs(const lmgc_model* m, const int32_t* tok, int B, int W, const lmgc_serial_params* p,
                      uint32_t total, uint32_t* cdf, float* logp, void* ws, size_t ws_bytes, hipStream_t s) {
   if (!m) return set_error(LMGC_EINVAL, "model is NULL");
@@ -406,109 +537,9 @@ static int run_probs(const lmgc_model* m, const int32_t* tok, int B, int W, cons
   ProbsWs w = carve(m, B, W, (char*)ws);
   if (ws_bytes < w.bytes) return set_error(LMGC_ESIZE, "workspace too small: %zu < %zu", ws_bytes, w.bytes);
 
-  const int M = B * W, d = c.d_model, hd = m->hd, F = c.d_ff;
-  const bool bf = c.dtype == LMGC_DTYPE_BF16;
-  const bool llama = c.arch == LMGC_ARCH_LLAMA;
-  auto gemm = [&](const void* A, const void* Bw, int Npad, int K, const EpiArgs& e) {
-    return bf ? launch_gemm_bf16((const uint16_t*)A, (const uint16_t*)Bw, M, Npad, K, e, s)
-              : launch_gemm_f32((const float*)A, (const float*)Bw, M, Npad, K, e, s);
-  };
-  {
-    ScopedTimer t(LMGC_K_EMBED, s);
-    HIP_OK(launch_embed(tok, B, W, p->bos_id, m->tok_emb, m->pos_emb, d, c.vocab, c.dtype, w.h, s));
-  }
-  for (int l = 0; l < c.n_layers; l++) {
-    const Layer& L = m->layers[l];
-    {
-      ScopedTimer t(LMGC_K_NORM, s);
-      HIP_OK(launch_norm(w.h, M, d, L.n1, L.n1b, !llama, c.norm_eps, c.dtype, w.a, s));
-    }
-    {
-      ScopedTimer t(LMGC_K_GEMM_QKV, s);
-      EpiArgs e = {};
-      e.kind = llama ? EPI_QKV_ROPE : EPI_QKV_BIAS;
-      e.M = M;
-      e.N = m->n_qkv;
-      e.bias = L.bqkv;
-      e.q = w.q;
-      e.k = w.k;
-      e.v = w.v;
-      e.W = W;
-      e.Hq = c.n_heads;
-      e.Hkv = c.n_kv_heads;
-      e.hd = hd;
-      e.rope = m->rope;
-      HIP_OK(gemm(w.a, L.wqkv, m->n_qkv_pad, d, e));
-    }
-    {
-      ScopedTimer t(LMGC_K_ATTN, s);
-      if (bf)
-        HIP_OK(launch_attention_bf16((const uint16_t*)w.q, (const uint16_t*)w.k, (const uint16_t*)w.v,
-                                     (uint16_t*)w.o, B, c.n_heads, c.n_kv_heads, W, hd, s));
-      else
-        HIP_OK(launch_attention_f32((const float*)w.q, (const float*)w.k, (const float*)w.v, (float*)w.o, B,
-                                    c.n_heads, c.n_kv_heads, W, hd, s));
-    }
-    {
-      ScopedTimer t(LMGC_K_GEMM_O, s);
-      EpiArgs e = {};
-      e.kind = EPI_RESID;
-      e.M = M;
-      e.N = d;
-      e.c = w.h;
-      e.ldc = d;
-      e.bias = L.bo;
-      HIP_OK(gemm(w.o, L.wo, m->d_pad, c.n_heads * hd, e));
-    }
-    {
-      ScopedTimer t(LMGC_K_NORM, s);
-      HIP_OK(launch_norm(w.h, M, d, L.n2, L.n2b, !llama, c.norm_eps, c.dtype, w.a, s));
-    }
-    {
-      ScopedTimer t(LMGC_K_GEMM_UP, s);
-      EpiArgs e = {};
-      e.kind = llama ? EPI_SWIGLU : EPI_BIAS_GELU;
-      e.M = M;
-      e.N = m->n_up;
-      e.bias = L.bup;
-      e.out = w.ff;
-      e.ld_out = F;
-      HIP_OK(gemm(w.a, L.wup, m->n_up_pad, d, e));
-    }
-    {
-      ScopedTimer t(LMGC_K_GEMM_DOWN, s);
-      EpiArgs e = {};
-      e.kind = EPI_RESID;
-      e.M = M;
-      e.N = d;
-      e.c = w.h;
-      e.ldc = d;
-      e.bias = L.bdown;
-      HIP_OK(gemm(w.ff, L.wdown, m->d_pad, F, e));
-    }
-  }
-  {
-    ScopedTimer t(LMGC_K_NORM, s);
-    HIP_OK(launch_norm(w.h, M, d, m->final_g, m->final_b, !llama, c.norm_eps, c.dtype, w.a, s));
-  }
-  {
-    ScopedTimer t(LMGC_K_GEMM_HEAD, s);
-    EpiArgs e = {};
-    e.kind = EPI_STORE_F32;
-    e.M = M;
-    e.N = c.vocab;
-    e.c = w.logits;
-    e.ldc = m->v_pad;
-    HIP_OK(gemm(w.a, m->head, m->v_pad, d, e));
-  }
-  {
-    ScopedTimer t(LMGC_K_LSE_CDF, s);
-    int32_t ids[LMGC_NALPHA];
-    for (int i = 0; i < 16; i++) ids[i] = p->hex_ids[i];
-    ids[16] = p->sep_id;
-    HIP_OK(launch_lse_cdf(w.logits, M, m->v_pad, c.vocab, ids, total, cdf, logp, s));
-  }
-  return LMGC_OK;
+  std::vector<void*> kc(c.n_layers, w.k), vc(c.n_layers, w.v);
+  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.logits, kc.data(), vc.data()};
+  return forward(m, tok, B, W, -1, p, total, f, cdf, logp, s);
 }
 
 static double probs_flops(const lmgc_model* m, int B, int W, int kind) {
@@ -527,6 +558,95 @@ static double probs_flops(const lmgc_model* m, int B, int W, int kind) {
 }
 
 // ------------------------------------------------------------ codec driver
+// --------------------------------------------------- decoding-step workspace
+// One decoding step works on compact rows (one per window) and keeps every
+// layer's K and V of the window group in a cache; q keeps the [B, Hq, W, hd]
+// layout the attention kernel reads (only the current position is written).
+constexpr int kStepMaxB = 16;
+
+struct StepWs {
+  float* h;
+  void *a, *q, *o, *ff;
+  float* logits;
+  int32_t* tok;     // [B] input token of the step (the previous position's)
+  uint32_t* cdf;    // [B, 19]
+  float* logp;      // [B, 17]
+  char* zero_from;  // q and the caches: cleared for every window group
+  size_t zero_bytes, bytes;
+  std::vector<void*> kc, vc;
+};
+
+static StepWs carve_step(const lmgc_model* m, int B, int W, char* base) {
+  const lmgc_model_config& c = m->cfg;
+  StepWs w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* p = base ? base + off : nullptr;
+    off = align_up(off + bytes, 256);
+    return p;
+  };
+  const size_t act = m->act, hq = (size_t)c.n_heads * m->hd, hkv = (size_t)c.n_kv_heads * m->hd;
+  w.h = (float*)take((size_t)B * c.d_model * 4);
+  w.a = take((size_t)B * std::max<size_t>(c.d_model, hq) * act);
+  w.o = take((size_t)B * hq * act);
+  w.ff = take((size_t)B * c.d_ff * act);
+  w.logits = (float*)take((size_t)B * m->v_pad * 4);
+  w.tok = (int32_t*)take((size_t)B * 4);
+  w.cdf = (uint32_t*)take((size_t)B * (LMGC_NSYM + 1) * 4);
+  w.logp = (float*)take((size_t)B * LMGC_NALPHA * 4);
+  const size_t z0 = off;
+  w.q = take((size_t)B * W * hq * act);
+  for (int l = 0; l < c.n_layers; l++) {
+    w.kc.push_back(take((size_t)B * W * hkv * act));
+    w.vc.push_back(take((size_t)B * W * hkv * act));
+  }
+  w.zero_from = base ? base + z0 : nullptr;
+  w.zero_bytes = off - z0;
+  w.bytes = off;
+  return w;
+}
+
+static int check_step(const lmgc_model* m, int B, int W, const lmgc_serial_params* p, uint32_t total) {
+  if (!m) return set_error(LMGC_EINVAL, "model is NULL");
+  int rc = check_serial(p, m->cfg.vocab);
+  if (rc) return rc;
+  if (B <= 0 || B > kStepMaxB || W <= 0) return set_error(LMGC_EINVAL, "need 0 < B <= %d and W > 0", kStepMaxB);
+  if (W > m->cfg.max_pos) return set_error(LMGC_EINVAL, "W=%d exceeds the model's max_pos=%d", W, m->cfg.max_pos);
+  if (m->cfg.dtype == LMGC_DTYPE_BF16 && W % 8) return set_error(LMGC_EUNSUPPORTED, "bf16 models need W %% 8 == 0");
+  if (total < 2 * LMGC_NSYM || total > (1u << 24)) return set_error(LMGC_EINVAL, "total must be in [36, 2^24]");
+  return LMGC_OK;
+}
+
+// One decoding step at position j of every window of the group (w.tok holds
+// the tokens at j - 1); tables land in w.cdf (and w.logp).
+static int run_step(const lmgc_model* m, StepWs& w, int B, int W, int j, const lmgc_serial_params* p,
+                    uint32_t total, bool want_logp, hipStream_t s) {
+  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.logits, w.kc.data(), w.vc.data()};
+  return forward(m, w.tok, B, W, j, p, total, f, w.cdf, want_logp ? w.logp : nullptr, s);
+}
+
+// lmgc_probs computed one position at a time through the cache, with the
+// given tokens as the decoded prefix.
+static int run_stepwise(const lmgc_model* m, const int32_t* tok, int B, int W, const lmgc_serial_params* p,
+                        uint32_t total, uint32_t* cdf, float* logp, void* ws, size_t ws_bytes, hipStream_t s) {
+  int rc = check_step(m, B, W, p, total);
+  if (rc) return rc;
+  if (!tok || !cdf || !ws) return set_error(LMGC_EINVAL, "NULL device buffer");
+  StepWs w = carve_step(m, B, W, (char*)ws);
+  if (ws_bytes < w.bytes) return set_error(LMGC_ESIZE, "workspace too small: %zu < %zu", ws_bytes, w.bytes);
+  HIP_OK(hipMemsetAsync(w.zero_from, 0, w.zero_bytes, s));
+  for (int j = 0; j < W; j++) {
+    if (j > 0) HIP_OK(hipMemcpy2DAsync(w.tok, 4, tok + (j - 1), (size_t)W * 4, 4, B, hipMemcpyDeviceToDevice, s));
+    if ((rc = run_step(m, w, B, W, j, p, total, logp != nullptr, s))) return rc;
+    HIP_OK(hipMemcpy2DAsync(cdf + (size_t)j * (LMGC_NSYM + 1), (size_t)W * (LMGC_NSYM + 1) * 4, w.cdf,
+                            (LMGC_NSYM + 1) * 4, (LMGC_NSYM + 1) * 4, B, hipMemcpyDeviceToDevice, s));
+    if (logp)
+      HIP_OK(hipMemcpy2DAsync(logp + (size_t)j * LMGC_NALPHA, (size_t)W * LMGC_NALPHA * 4, w.logp, LMGC_NALPHA * 4,
+                              LMGC_NALPHA * 4, B, hipMemcpyDeviceToDevice, s));
+  }
+  return LMGC_OK;
+}
+
 struct CodecWs {
   int32_t* tok;
   uint8_t* sym;
@@ -659,8 +779,10 @@ static int decode(const lmgc_model* m, const uint8_t* buf, size_t bytes, int32_t
   if ((rc = check_serial(&h.p, m->cfg.vocab))) return rc;
   const int W = h.p.window;
   const int64_t nt = num_tokens(h.n_values, h.p);
-  CodecWs cw = carve_codec(m, B, W, (char*)ws);
-  if (ws_bytes < cw.bytes) return set_error(LMGC_ESIZE, "codec workspace too small: %zu < %zu", ws_bytes, cw.bytes);
+  const int G = std::min(B, kStepMaxB);  // windows decoded together
+  if ((rc = check_step(m, G, W, &h.p, h.total))) return rc;
+  StepWs sw = carve_step(m, G, W, (char*)ws);
+  if (ws_bytes < sw.bytes) return set_error(LMGC_ESIZE, "codec workspace too small: %zu < %zu", ws_bytes, sw.bytes);
   std::vector<uint32_t> bits(h.n_windows);
   memcpy(bits.data(), buf + LMGC_HEADER_BYTES, 4 * (size_t)h.n_windows);
   std::vector<size_t> off(h.n_windows + 1);
@@ -672,12 +794,14 @@ static int decode(const lmgc_model* m, const uint8_t* buf, size_t bytes, int32_t
   std::vector<int32_t> id_of(LMGC_NALPHA);
   for (int i = 0; i < 16; i++) id_of[i] = h.p.hex_ids[i];
   id_of[16] = h.p.sep_id;
-  std::vector<uint32_t> rows((size_t)B * (LMGC_NSYM + 1));
-  std::vector<int32_t> col(B);
-  std::vector<int32_t> pad((size_t)B * W, h.p.pad_id);
-  std::vector<lmgc_decoder> dec(B);
-  for (int64_t w0 = 0; w0 < h.n_windows; w0 += B) {
-    const int nb = (int)std::min<int64_t>(B, h.n_windows - w0);
+  std::vector<uint32_t> rows((size_t)G * (LMGC_NSYM + 1));
+  std::vector<int32_t> col(G);
+  std::vector<lmgc_decoder> dec(G);
+  // Window groups, token by token from BOS: one decoding step gives every
+  // window of the group the table of its next position, the host decodes
+  // the symbols, and their tokens are the next step's input.
+  for (int64_t w0 = 0; w0 < h.n_windows; w0 += G) {
+    const int nb = (int)std::min<int64_t>(G, h.n_windows - w0);
     std::vector<int> len(nb);
     int maxlen = 0;
     for (int i = 0; i < nb; i++) {
@@ -685,11 +809,10 @@ static int decode(const lmgc_model* m, const uint8_t* buf, size_t bytes, int32_t
       maxlen = std::max(maxlen, len[i]);
       decoder_init(&dec[i], buf + off[w0 + i], bits[w0 + i]);
     }
-    HIP_OK(hipMemcpyAsync(cw.tok, pad.data(), (size_t)nb * W * 4, hipMemcpyHostToDevice, s));
+    HIP_OK(hipMemsetAsync(sw.zero_from, 0, sw.zero_bytes, s));
     for (int j = 0; j < maxlen; j++) {
-      if ((rc = run_probs(m, cw.tok, nb, W, &h.p, h.total, cw.cdf, nullptr, cw.probs, cw.probs_bytes, s))) return rc;
-      HIP_OK(hipMemcpy2DAsync(rows.data(), (LMGC_NSYM + 1) * 4, cw.cdf + (size_t)j * (LMGC_NSYM + 1),
-                              (size_t)W * (LMGC_NSYM + 1) * 4, (LMGC_NSYM + 1) * 4, nb, hipMemcpyDeviceToHost, s));
+      if ((rc = run_step(m, sw, nb, W, j, &h.p, h.total, false, s))) return rc;
+      HIP_OK(hipMemcpyAsync(rows.data(), sw.cdf, (size_t)nb * (LMGC_NSYM + 1) * 4, hipMemcpyDeviceToHost, s));
       HIP_OK(hipStreamSynchronize(s));
       for (int i = 0; i < nb; i++) {
         col[i] = h.p.pad_id;
@@ -701,7 +824,7 @@ static int decode(const lmgc_model* m, const uint8_t* buf, size_t bytes, int32_t
         sym[(size_t)(w0 + i) * W + j] = (uint8_t)b;
         col[i] = id_of[b];
       }
-      HIP_OK(hipMemcpy2DAsync(cw.tok + j, (size_t)W * 4, col.data(), 4, 4, nb, hipMemcpyHostToDevice, s));
+      HIP_OK(hipMemcpyAsync(sw.tok, col.data(), (size_t)nb * 4, hipMemcpyHostToDevice, s));
     }
   }
   HIP_OK(hipStreamSynchronize(s));
@@ -835,7 +958,20 @@ size_t lmgc_container_bound(int64_t n_values, const lmgc_serial_params* p) {
 size_t lmgc_codec_workspace(const lmgc_model* m, int64_t n_values, const lmgc_serial_params* p, int32_t batch) {
   (void)n_values;
   if (!m || !p || batch <= 0 || p->window <= 0) return 0;
-  return carve_codec(m, batch, p->window, nullptr).bytes;
+  return std::max(carve_codec(m, batch, p->window, nullptr).bytes,
+                  carve_step(m, std::min(batch, kStepMaxB), p->window, nullptr).bytes);
+}
+
+size_t lmgc_step_workspace(const lmgc_model* m, int32_t B, int32_t W) {
+  if (!m || B <= 0 || B > kStepMaxB || W <= 0) return 0;
+  return carve_step(m, B, W, nullptr).bytes;
+}
+
+int lmgc_probs_stepwise(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t W,
+                        const lmgc_serial_params* p, uint32_t total, uint32_t* d_cdf, float* d_logp, void* d_ws,
+                        size_t ws_bytes, void* stream) {
+  clear_error();
+  return run_stepwise(m, d_tokens, B, W, p, total, d_cdf, d_logp, d_ws, ws_bytes, (hipStream_t)stream);
 }
 
 int lmgc_compress(const lmgc_model* m, const void* d_values, int64_t n_values, const lmgc_serial_params* p,
@@ -887,7 +1023,7 @@ int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint1
   if (!d_q || !d_k || !d_vt || !d_o || B <= 0 || W <= 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv)
     return set_error(LMGC_EINVAL, "bad arguments");
   if ((hd != 64 && hd != 128) || W % 8) return set_error(LMGC_EUNSUPPORTED, "need hd in {64, 128} and W %% 8 == 0");
-  hipError_t err = launch_attention_bf16(d_q, d_k, d_vt, d_o, B, Hq, Hkv, W, hd, (hipStream_t)stream);
+  hipError_t err = launch_attention_bf16(d_q, d_k, d_vt, d_o, B, Hq, Hkv, W, hd, -1, (hipStream_t)stream);
   if (err != hipSuccess) return set_error(LMGC_EDEVICE, "attention launch: %s", hipGetErrorString(err));
   return LMGC_OK;
 }

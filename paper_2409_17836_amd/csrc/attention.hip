@@ -77,7 +77,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
                                                            const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ vt,
                                                            uint16_t* __restrict__ o, int Hq,
-                                                           int Hkv, int W, float sl2) {
+                                                           int Hkv, int W, float sl2, int dq) {
   constexpr int BQ = 128, BKV = 64, KCH = HD / 8, NKS = HD / 16, NOB = HD / 32;
   constexpr int KROWS = 1024 / (HD * 2);          // K rows per 1 KB direct load
   constexpr int NKL = BKV * HD * 2 / 1024 / 4;    // direct K loads per wave and tile
@@ -86,7 +86,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   __shared__ u32x4 sV0[HD * 8], sV1[HD * 8];  // V^T: [dim][64 keys]
 
   const int nqb = (W + BQ - 1) / BQ;
-  const int qb = nqb - 1 - (int)blockIdx.x;  // longest blocks first
+  // longest blocks first; a decoding step (dq >= 0) runs only dq's block
+  const int qb = dq >= 0 ? dq / BQ : nqb - 1 - (int)blockIdx.x;
   const int h = blockIdx.y, b = blockIdx.z;
   const int kvh = h * Hkv / Hq;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -310,9 +311,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   if (t < ntiles) step(t, sa0, sa1, sb0, sb1, sK1, sV0, sK0, sV1);
 
   l_i += __shfl_xor(l_i, 32, 64);
-  if (myq < W) {
+  if (dq >= 0 ? myq == dq : myq < W) {
     const float inv = 1.0f / l_i;
-    uint16_t* orow = o + ((int64_t)b * W + myq) * (int64_t)(Hq * HD) + h * HD;
+    uint16_t* orow = o + ((int64_t)b * (dq >= 0 ? 1 : W) + (dq >= 0 ? 0 : myq)) * (int64_t)(Hq * HD) + h * HD;
 #pragma unroll
     for (int i = 0; i < NOB; i++) {
 #pragma unroll
@@ -334,12 +335,13 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
                                                       const float* __restrict__ k,
                                                       const float* __restrict__ v,
                                                       float* __restrict__ o, int Hq, int Hkv,
-                                                      int W, float scale) {
+                                                      int W, float scale, int dq) {
   __shared__ float sK[64][HD + 1];
   __shared__ float sV[64][HD + 1];
   const int h = blockIdx.y, b = blockIdx.z;
   const int kvh = h * Hkv / Hq;
-  const int myq = blockIdx.x * 64 + threadIdx.x;
+  const int qblk = dq >= 0 ? dq / 64 : (int)blockIdx.x;  // a decoding step: dq's block only
+  const int myq = qblk * 64 + threadIdx.x;
   const float* Qp = q + (int64_t)(b * Hq + h) * W * HD;
   const float* Kp = k + (int64_t)(b * Hkv + kvh) * W * HD;
   const float* Vp = v + (int64_t)(b * Hkv + kvh) * W * HD;
@@ -351,7 +353,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
     acc[i] = 0.f;
   }
   float m = -INFINITY, l = 0.f;
-  const int kend = min(W, (int)blockIdx.x * 64 + 64);
+  const int kend = min(W, qblk * 64 + 64);
   for (int k0 = 0; k0 < kend; k0 += 64) {
     __syncthreads();
     for (int c = threadIdx.x; c < 64 * HD; c += 64) {
@@ -377,8 +379,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
       m = mn;
     }
   }
-  if (myq < W) {
-    float* orow = o + ((int64_t)b * W + myq) * (int64_t)(Hq * HD) + h * HD;
+  if (dq >= 0 ? myq == dq : myq < W) {
+    float* orow = o + ((int64_t)b * (dq >= 0 ? 1 : W) + (dq >= 0 ? 0 : myq)) * (int64_t)(Hq * HD) + h * HD;
 #pragma unroll
     for (int i = 0; i < HD; i++) orow[i] = acc[i] / l;
   }
@@ -387,16 +389,16 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 }  // namespace
 
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
-                                 uint16_t* o, int B, int Hq, int Hkv, int W, int hd,
+                                 uint16_t* o, int B, int Hq, int Hkv, int W, int hd, int dq,
                                  hipStream_t s) {
   if (B <= 0 || W <= 0) return hipSuccess;
-  if (W % 8) return hipErrorInvalidValue;
-  const dim3 grid((W + 127) / 128, Hq, B), block(256);
+  if (W % 8 || dq >= W) return hipErrorInvalidValue;
+  const dim3 grid(dq >= 0 ? 1 : (W + 127) / 128, Hq, B), block(256);
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)hd));
   if (hd == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2);
+    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);
   else if (hd == 64)
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2);
+    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -404,22 +406,23 @@ hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uin
 
 
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o, int B,
-                                int Hq, int Hkv, int W, int hd, hipStream_t s) {
+                                int Hq, int Hkv, int W, int hd, int dq, hipStream_t s) {
   if (B <= 0 || W <= 0) return hipSuccess;
-  const dim3 grid((W + 63) / 64, Hq, B), block(64);
+  if (dq >= W) return hipErrorInvalidValue;
+  const dim3 grid(dq >= 0 ? 1 : (W + 63) / 64, Hq, B), block(64);
   const float scale = (float)(1.0 / sqrt((double)hd));
   switch (hd) {
     case 16:
-      hipLaunchKernelGGL(attn_f32_kernel<16>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, scale);
+      hipLaunchKernelGGL(attn_f32_kernel<16>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, scale, dq);
       break;
     case 32:
-      hipLaunchKernelGGL(attn_f32_kernel<32>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, scale);
+      hipLaunchKernelGGL(attn_f32_kernel<32>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, scale, dq);
       break;
     case 48:
-      hipLaunchKernelGGL(attn_f32_kernel<48>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, scale);
+      hipLaunchKernelGGL(attn_f32_kernel<48>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, scale, dq);
       break;
     case 64:
-      hipLaunchKernelGGL(attn_f32_kernel<64>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, scale);
+      hipLaunchKernelGGL(attn_f32_kernel<64>, grid, block, 0, s, q, k, v, o, Hq, Hkv, W, scale, dq);
       break;
     default:
       return hipErrorInvalidValue;

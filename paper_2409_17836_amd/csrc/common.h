@@ -52,6 +52,10 @@ struct EpiArgs {
   void* v;
   int W, Hq, Hkv, hd;
   const float2* rope;  // [max_pos, hd/2] (cos, sin)
+  // row -> (window, position): step == 0 (the zero-initialised default): row
+  // r is position r % W of window r / W (a batch of whole windows); step != 0:
+  // row r is window r at position dpos (one decoding step)
+  int step, dpos;
   // SWIGLU / GELU output
   void* out;           // [M, ld_out]
   int ld_out;
@@ -64,8 +68,12 @@ hipError_t launch_serialize(const void* values, int64_t n_values, const lmgc_ser
                             uint8_t* sym, hipStream_t s);
 
 // Token ids outside [0, vocab) are clamped (callers validate them).
+// dpos < 0: rows b*W + j of B whole windows (token of row j is BOS for j = 0,
+// else tokens[b, j-1]); dpos >= 0: row b is window b at position dpos, whose
+// input token is BOS for dpos = 0, else tokens[b].
 hipError_t launch_embed(const int32_t* tokens, int B, int W, int bos_id, const void* tok_emb,
-                        const void* pos_emb, int d, int vocab, int dtype, float* h, hipStream_t s);
+                        const void* pos_emb, int d, int vocab, int dtype, int dpos, float* h,
+                        hipStream_t s);
 
 // y = norm(h) (rms if ln_bias == nullptr && !layernorm) in model dtype.
 hipError_t launch_norm(const float* h, int M, int d, const void* gain, const void* bias,
@@ -75,12 +83,18 @@ hipError_t launch_gemm_bf16(const uint16_t* A, const uint16_t* B, int M, int N_p
                             const EpiArgs& e, hipStream_t s);
 hipError_t launch_gemm_f32(const float* A, const float* B, int M, int N_pad, int K,
                            const EpiArgs& e, hipStream_t s);
+// Decoding step: M <= 16 rows, each output element accumulated exactly as
+// launch_gemm_bf16 accumulates it (same MFMA, operand layout and k order).
+hipError_t launch_gemm_bf16_rows(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
+                                 const EpiArgs& e, hipStream_t s);
 
+// dq < 0: all queries of B windows, o [B*W, Hq*hd].  dq >= 0: only query dq
+// of each window (same per-query arithmetic), o [B, Hq*hd].
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* vt,
-                                 uint16_t* o, int B, int Hq, int Hkv, int W, int hd,
+                                 uint16_t* o, int B, int Hq, int Hkv, int W, int hd, int dq,
                                  hipStream_t s);
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,
-                                int B, int Hq, int Hkv, int W, int hd, hipStream_t s);
+                                int B, int Hq, int Hkv, int W, int hd, int dq, hipStream_t s);
 
 // logits [M, ldz] (first V valid) -> cdf [M, 19], logp [M, 17] (nullable);
 // alpha_ids is a host array of the 17 alphabet token ids.

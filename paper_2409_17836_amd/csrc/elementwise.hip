@@ -33,15 +33,18 @@ __device__ inline float load_param(const void* p, int i, int dtype) {
 }
 
 // ------------------------------------------------------------------ embed
-// h[b*W + j, :] = E[x] (+ P[j]) with x = BOS for j = 0, else tokens[b, j-1].
+// h[b*W + j, :] = E[x] (+ P[j]) with x = BOS for j = 0, else tokens[b, j-1];
+// a decoding step (dpos >= 0): h[b, :] for position dpos, x = BOS for
+// dpos = 0, else tokens[b].
 __global__ void embed_kernel(const int32_t* __restrict__ tokens, int B, int W, int bos,
                              const void* __restrict__ E, const void* __restrict__ P, int d,
-                             int V, int dtype, float* __restrict__ h) {
+                             int V, int dtype, int dpos, float* __restrict__ h) {
   const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
-  if (row >= (int64_t)B * W) return;
-  const int j = (int)(row % W);
-  const int x = min(max(j == 0 ? bos : tokens[row - 1], 0), V - 1);
+  if (row >= (dpos >= 0 ? (int64_t)B : (int64_t)B * W)) return;
+  const int j = dpos >= 0 ? dpos : (int)(row % W);
+  const int prev = j == 0 ? bos : (dpos >= 0 ? tokens[row] : tokens[row - 1]);
+  const int x = min(max(prev, 0), V - 1);
   float* out = h + row * d;
   for (int c = lane * 4; c < d; c += kWave * 4) {
     float4 v;
@@ -246,10 +249,11 @@ __global__ void gather_rows_kernel(GatherSrcs srcs, const int32_t* __restrict__ 
 }  // namespace
 
 hipError_t launch_embed(const int32_t* tokens, int B, int W, int bos_id, const void* tok_emb,
-                        const void* pos_emb, int d, int vocab, int dtype, float* h, hipStream_t s) {
-  const int64_t rows = (int64_t)B * W;
+                        const void* pos_emb, int d, int vocab, int dtype, int dpos, float* h,
+                        hipStream_t s) {
+  const int64_t rows = dpos >= 0 ? (int64_t)B : (int64_t)B * W;
   hipLaunchKernelGGL(embed_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, tokens,
-                     B, W, bos_id, tok_emb, pos_emb, d, vocab, dtype, h);
+                     B, W, bos_id, tok_emb, pos_emb, d, vocab, dtype, dpos, h);
   return hipGetLastError();
 }
 

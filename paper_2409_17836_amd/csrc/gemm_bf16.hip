@@ -228,6 +228,112 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   }
 }
 
+// Decoding step (M <= 16 rows: one row per window).  A workgroup of four
+// waves owns 64 columns; wave w accumulates the 16-column block c + 16 w and
+// runs, for every output element, the same chain as gemm_bf16_kernel:
+// 16x16x32 bf16 MFMAs over the 32-wide k chunks in increasing order, lane l
+// holding row (l & 15) and k values 8*(l >> 4) .. +8 of a chunk.  So a row's
+// outputs equal, bit for bit, what the tiled kernel gives that row in a
+// batch of whole windows.  Operands come straight from global memory (the
+// step streams the weights once, one block per wave for parallelism),
+// kRowsPf chunks ahead.  Blocks 2 and 3 hand their accumulators to blocks 0
+// and 1 through LDS, which run the epilogue on the (col, col + 32) pairs.
+constexpr int kRowsPf = 16;
+
+template <int KIND, int HD>
+__global__ __launch_bounds__(256) void gemm_bf16_rows_kernel(const uint16_t* __restrict__ A,
+                                                             const uint16_t* __restrict__ Bw, int M,
+                                                             int K, EpiArgs e) {
+  __shared__ f32x4 part[2][64];  // accumulators of blocks 2 and 3
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + wave * 16;  // this wave's block
+  const int r = lane & 15, kq = lane >> 4;
+  // rows past M re-read row M - 1; they only feed outputs that are not stored
+  const u32x4* pa = reinterpret_cast<const u32x4*>(A + (int64_t)min(r, M - 1) * K + kq * 8);
+  const u32x4* pb = reinterpret_cast<const u32x4*>(Bw + (int64_t)(c + r) * K + kq * 8);
+  f32x4 acc = f32x4{};
+  const int nkc = K / 32;  // chunk kc starts at u32x4 index 4 * kc
+  u32x4 fa[kRowsPf], fb[kRowsPf];
+  auto fetch = [&](int u, int kc) __attribute__((always_inline)) {
+    fa[u] = pa[4 * kc];
+    fb[u] = pb[4 * kc];
+  };
+  auto mma = [&](int u) __attribute__((always_inline)) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[u]), as_bf16x8(fb[u]), acc, 0, 0, 0);
+  };
+  // chunk kc lives in slot kc % kRowsPf.  The steady loop consumes and
+  // refills every slot without conditions (so the loads' wait counts stay
+  // exact); the last chunks drain afterwards.
+  if (nkc >= kRowsPf) {
+#pragma unroll
+    for (int u = 0; u < kRowsPf; u++) fetch(u, u);
+    int kc0 = 0;
+    for (; kc0 + 2 * kRowsPf <= nkc; kc0 += kRowsPf) {
+#pragma unroll
+      for (int u = 0; u < kRowsPf; u++) {
+        mma(u);
+        fetch(u, kc0 + kRowsPf + u);
+      }
+    }
+    const int rest = nkc - kc0 - kRowsPf;  // chunks after the loaded ones, < kRowsPf
+#pragma unroll
+    for (int u = 0; u < kRowsPf; u++) {
+      mma(u);
+      if (u < rest) fetch(u, kc0 + kRowsPf + u);
+    }
+#pragma unroll
+    for (int u = 0; u < kRowsPf; u++)
+      if (u < rest) mma(u);
+  } else {
+    for (int kc = 0; kc < nkc; kc++) {
+      fetch(0, kc);
+      mma(0);
+    }
+  }
+  if (wave >= 2) part[wave - 2][lane] = acc;
+  __syncthreads();
+  if (wave >= 2) return;
+  const f32x4 hi = part[wave][lane];  // block c + 32, same lane layout
+  // lane holds column c + (lane & 15) (paired with + 32) and rows 4 kq + i
+  using E = Epi<uint16_t, KIND, HD>;
+  const int col = c + r;
+  const ColInfo ci = E::column(e, col);
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const int row = 4 * kq + i;
+    if (row < M) E::row(e, ci, col, row, row, e.dpos, acc[i], hi[i]);
+  }
+}
+
+template <int HD>
+hipError_t launch_rows_kind(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
+                            const EpiArgs& e, hipStream_t s) {
+  const dim3 grid(N_pad / 64), block(256);  // 4 waves x 16 columns
+  switch (e.kind) {
+    case EPI_STORE_F32:
+      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_STORE_F32, HD>), grid, block, 0, s, A, B, M, K, e);
+      break;
+    case EPI_RESID:
+      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_RESID, HD>), grid, block, 0, s, A, B, M, K, e);
+      break;
+    case EPI_QKV_ROPE:
+      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_QKV_ROPE, HD>), grid, block, 0, s, A, B, M, K, e);
+      break;
+    case EPI_QKV_BIAS:
+      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_QKV_BIAS, HD>), grid, block, 0, s, A, B, M, K, e);
+      break;
+    case EPI_SWIGLU:
+      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_SWIGLU, HD>), grid, block, 0, s, A, B, M, K, e);
+      break;
+    case EPI_BIAS_GELU:
+      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_BIAS_GELU, HD>), grid, block, 0, s, A, B, M, K, e);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <int HD>
 hipError_t launch_kind(const uint16_t* A, const uint16_t* B, int M, int K, int ntm, int ntn,
                        const EpiArgs& e, hipStream_t s) {
@@ -260,10 +366,21 @@ hipError_t launch_kind(const uint16_t* A, const uint16_t* B, int M, int K, int n
 
 }  // namespace
 
+hipError_t launch_gemm_bf16_rows(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
+                                 const EpiArgs& e, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (M > 16 || !e.step || K % BK != 0 || N_pad % BN != 0) return hipErrorInvalidValue;
+  const bool qkv = e.kind == EPI_QKV_ROPE || e.kind == EPI_QKV_BIAS;
+  if (qkv && e.hd == 128) return launch_rows_kind<128>(A, B, M, N_pad, K, e, s);
+  if (qkv && e.hd == 64) return launch_rows_kind<64>(A, B, M, N_pad, K, e, s);
+  if (qkv) return hipErrorInvalidValue;
+  return launch_rows_kind<0>(A, B, M, N_pad, K, e, s);
+}
+
 hipError_t launch_gemm_bf16(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
                             const EpiArgs& e, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (K % BK != 0 || N_pad % BN != 0) return hipErrorInvalidValue;
+  if (e.step || K % BK != 0 || N_pad % BN != 0) return hipErrorInvalidValue;
   const int ntm = (M + BM - 1) / BM, ntn = N_pad / BN;
   const bool qkv = e.kind == EPI_QKV_ROPE || e.kind == EPI_QKV_BIAS;
   if (qkv && e.hd == 128) return launch_kind<128>(A, B, M, K, ntm, ntn, e, s);

@@ -2,7 +2,8 @@
 // the same fused epilogues as the bf16 kernel.  A plain LDS-tiled FMA kernel
 // (64 x 64 tile, 256 threads, 4 x 4 outputs per thread); every output is a
 // sequential k-ordered FMA chain, so results do not depend on M or on other
-// rows.  Used for the small float32 model, where the work is latency-bound.
+// rows (a decoding step runs it on one row per window and gets the same
+// values).  Used for the small float32 model, where the work is latency-bound.
 #include "epilogue.h"
 
 namespace lmgc {
@@ -62,7 +63,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   for (int i = 0; i < 4; i++) {
     const int row = m0 + ty * 4 + i;
     if (row >= M) continue;
-    const int b = row / W, pos = row - b * W;
+    const int b = e.step ? row : row / W, pos = e.step ? e.dpos : row - b * W;
     E::row(e, ci0, n0 + tx, row, b, pos, acc[i][0], acc[i][2]);
     E::row(e, ci1, n0 + tx + 16, row, b, pos, acc[i][1], acc[i][3]);
   }
