@@ -53,20 +53,24 @@ const char* lmgc_version(void);
  * in Sec. 5.3).  The value vector is read as a stream of bytes, each value's
  * bytes most-significant first when msb_first=1 (sign/exponent digits lead,
  * like printf("%08x")) or in memory (little-endian) order when msb_first=0;
- * each byte gives two hex-digit tokens, high nibble first; a separator token
- * follows every bytes_per_group bytes and the last (possibly partial) group.
- * bytes_per_group = 0 means no separator (the paper's H_n).  With
- * bytes_per_value = bytes_per_group = 4 every float32 is 8 digits + 1
- * separator = 9 tokens.
+ * each byte gives two hex-digit tokens, high nibble first; the separator
+ * (sep_id, then sep2_id if >= 0) follows every bytes_per_group bytes and the
+ * last (possibly partial) group.  bytes_per_group = 0 means no separator (the
+ * paper's H_n).  The paper's separators (Sec. 5.2, Table 1) are one space
+ * (H_s), a comma (H_c), a semicolon (H_semi) or a comma and a space (H_c+s:
+ * sep_id = ',' and sep2_id = ' ').  With bytes_per_value = bytes_per_group =
+ * 4 every float32 is 8 digits + 1 separator = 9 tokens (10 with sep2_id).
  *
  * The stream is cut into consecutive windows of `window` tokens (the last
  * one shorter; its tail is filled with pad_id).  The model input of a window
  * is BOS followed by the window's tokens shifted by one, so position j is
  * predicted from BOS and tokens 0..j-1 (Eq. 2); BOS is never coded.
  *
- * Coder bins: 0..15 = hex digit value, 16 = separator, 17 = escape (the rest
- * of the vocabulary; never coded).  Token ids of bins 0..16 are hex_ids[] and
- * sep_id; all ids must be < the model's vocabulary.
+ * Coder bins: 0..15 = hex digit value, 16 = sep_id, then 17 = sep2_id when
+ * there is one, then the escape bin (the rest of the vocabulary; never
+ * coded).  The alphabet (bins before the escape) has A = 17 or 18 symbols
+ * (lmgc_alphabet_size); tables have A + 2 entries.  Alphabet ids must be
+ * pairwise distinct and, like bos_id and pad_id, < the model's vocabulary.
  */
 typedef struct {
   int32_t bytes_per_value; /* 4 (float32) | 2 | 1 (8-bit indices) */
@@ -77,10 +81,15 @@ typedef struct {
   int32_t pad_id;
   int32_t sep_id;
   int32_t hex_ids[16];
+  int32_t sep2_id;         /* second separator token, or -1 (none) */
 } lmgc_serial_params;
 
-#define LMGC_NALPHA 17 /* coded alphabet: 16 digits + separator   */
-#define LMGC_NSYM 18   /* coder bins: alphabet + escape            */
+#define LMGC_NALPHA 17     /* alphabet with one separator token        */
+#define LMGC_NALPHA_MAX 18 /* alphabet with two separator tokens        */
+#define LMGC_NSYM_MAX 19   /* coder bins incl. escape, at most          */
+
+/* Alphabet size A (17 or 18) of these parameters, or < 0 if invalid. */
+int32_t lmgc_alphabet_size(const lmgc_serial_params* p);
 
 /* Tokens in the serialised stream of n_values values (>= 0), or < 0 on error. */
 int64_t lmgc_num_tokens(int64_t n_values, const lmgc_serial_params* p);
@@ -168,17 +177,19 @@ size_t lmgc_probs_workspace(const lmgc_model* m, int32_t B, int32_t W);
 /*
  * The LM as the coder's model (Sec. 4, "Compression": P_AC = P_LM).
  * d_tokens: [B, W] int32 data tokens of B windows (the BOS shift is done
- * here).  For every window b and position j < W:
+ * here).  With A = lmgc_alphabet_size(p), for every window b and position
+ * j < W:
  *   lp[a]  = log p(alphabet token a | BOS, tokens[b, 0..j-1]), normalised
- *            over the whole vocabulary (float32, a = 0..16);
- *   f[a]   = 1 + floor(exp(lp[a]) * (total - 18)) (in double), the largest
- *            giving up any excess over total-1 (lowest index on ties);
- *   f[17]  = total - sum(f[0..16])  (escape bin, never coded);
- *   d_cdf[b, j, 0..18] = 0, f0, f0+f1, ..., total.
- * d_logp (nullable) receives lp as [B, W, 17] float32.
+ *            over the whole vocabulary (float32, a = 0..A-1);
+ *   f[a]   = 1 + floor(exp(lp[a]) * (total - (A+1))) (in double), the
+ *            largest giving up any excess over total-1 (lowest index on ties);
+ *   f[A]   = total - sum(f[0..A-1])  (escape bin, never coded);
+ *   d_cdf[b, j, 0..A+1] = 0, f0, f0+f1, ..., total.
+ * d_logp (nullable) receives lp as [B, W, A] float32.
  * Row (b, j) is a bitwise function of the weights and tokens[b, 0..j-1]
  * only: it does not depend on later tokens, on other windows, on B or on W.
- * total must be in [18*2, 2^24].  GPU, async.  Errors: EINVAL, ESIZE (ws).
+ * total must be in [2*LMGC_NSYM_MAX, 2^24].  GPU, async.  Errors: EINVAL,
+ * ESIZE (ws).
  */
 int lmgc_probs(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t W,
                const lmgc_serial_params* p, uint32_t total, uint32_t* d_cdf, float* d_logp,
@@ -237,9 +248,9 @@ int lmgc_decode_symbol(lmgc_decoder* st, const uint32_t* cdf_row, int32_t nsym,
  * Container (little-endian): 128-byte header
  *   0 "LMGC" | 4 u16 version=1 | 6 u16 header bytes=128 | 8 u64 model tag |
  *   16 u64 n_values | 24 u8 bytes_per_value | 25 u8 bytes_per_group |
- *   26 u8 msb_first | 27 u8 nsym=18 | 28 u32 W | 32 u32 total |
+ *   26 u8 msb_first | 27 u8 nsym (A + 1) | 28 u32 W | 32 u32 total |
  *   36 u32 n_windows | 40 i32 bos | 44 i32 pad | 48 i32 sep | 52 i32 hex[16] |
- *   116..127 zero
+ *   116 u32 sep2_id + 1 (0: none) | 120..127 zero
  * then u32 bits[n_windows], then the payloads, each ceil(bits/8) bytes.
  */
 #define LMGC_HEADER_BYTES 128

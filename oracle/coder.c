@@ -17,13 +17,14 @@
  *     in memory (little-endian) order with the high nibble of each byte first;
  *   - a separator follows every group of bytes_per_group bytes, including the
  *     last (possibly partial) group; bytes_per_group=0 means no separator;
- *   - bins 0..15 are the hex digits, bin 16 the separator, bin 17 an escape
+ *   - bins 0..15 are the hex digits, bin 16 the separator (bin 17 a second
+ *     separator token when the separator is two characters), then an escape
  *     bin that holds the probability of every other vocabulary entry and is
- *     never coded;
- *   - frequencies: f_a = 1 + floor(exp(lp_a) * (T - 18)), computed in double
- *     from the float32 log-probability; if the 17 frequencies sum past T-1
- *     the largest (lowest index on ties) gives up the excess; the escape bin
- *     takes T - sum;
+ *     never coded; A = 17 or 18 alphabet symbols;
+ *   - frequencies: f_a = 1 + floor(exp(lp_a) * (T - (A + 1))), computed in
+ *     double from the float32 log-probability; if the A frequencies sum past
+ *     T-1 the largest (lowest index on ties) gives up the excess; the escape
+ *     bin takes T - sum;
  *   - coder: 62-bit code values, E1/E2/E3 renormalisation with pending bits,
  *     flush = pending+1 then one bit chosen by low < quarter; bits are packed
  *     most significant first, the last byte padded with zero bits; the
@@ -34,20 +35,20 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define ORC_NALPHA 17 /* 16 hex digits + separator */
-#define ORC_NSYM 18   /* + escape */
+#define ORC_NSYM_MAX 19 /* 16 hex digits + up to two separator tokens + escape */
 
 /* ------------------------------------------------------------------------ */
 /* Serialisation                                                             */
 /* ------------------------------------------------------------------------ */
 
-/* Number of tokens a vector of n values serialises to. */
+/* Number of tokens a vector of n values serialises to (nsep separator
+ * tokens after each group). */
 int64_t orc_num_tokens(int64_t n_values, int32_t bytes_per_value,
-                       int32_t bytes_per_group) {
+                       int32_t bytes_per_group, int32_t nsep) {
   int64_t nbytes = n_values * (int64_t)bytes_per_value;
   int64_t ngroups = 0;
   if (bytes_per_group > 0) ngroups = (nbytes + bytes_per_group - 1) / bytes_per_group;
-  return 2 * nbytes + ngroups;
+  return 2 * nbytes + ngroups * nsep;
 }
 
 /* Byte k (0-based, in emission order) of value i. */
@@ -59,12 +60,14 @@ static uint8_t value_byte(const uint8_t* values, int64_t i, int32_t k,
 
 /*
  * Serialise n values (raw little-endian bytes, bpv bytes each) into a token
- * stream.  tokens[t] gets the token id, sym[t] the coder bin (0..16).
+ * stream.  tokens[t] gets the token id, sym[t] the coder bin: 0..15 digits,
+ * 16 the separator sep_id, 17 the second separator sep2_id (only when
+ * sep2_id >= 0; the comma-and-space separator of the paper's H_c+s).
  * Returns the number of tokens written.
  */
 int64_t orc_serialize(const uint8_t* values, int64_t n_values, int32_t bpv,
                       int32_t bpg, int32_t msb_first, const int32_t* hex_ids,
-                      int32_t sep_id, int32_t* tokens, uint8_t* sym) {
+                      int32_t sep_id, int32_t sep2_id, int32_t* tokens, uint8_t* sym) {
   int64_t t = 0;
   int64_t byte_no = 0; /* bytes emitted since the stream start */
   int64_t nbytes = n_values * (int64_t)bpv;
@@ -77,6 +80,7 @@ int64_t orc_serialize(const uint8_t* values, int64_t n_values, int32_t bpv,
       byte_no++;
       if (bpg > 0 && (byte_no % bpg == 0 || byte_no == nbytes)) {
         tokens[t] = sep_id; sym[t] = 16; t++;
+        if (sep2_id >= 0) { tokens[t] = sep2_id; sym[t] = 17; t++; }
       }
     }
   }
@@ -89,9 +93,9 @@ int64_t orc_serialize(const uint8_t* values, int64_t n_values, int32_t bpv,
  * Returns 0 on success, -1 if the stream is malformed.
  */
 int orc_deserialize(const uint8_t* sym, int64_t n_tokens, int64_t n_values,
-                    int32_t bpv, int32_t bpg, int32_t msb_first,
+                    int32_t bpv, int32_t bpg, int32_t msb_first, int32_t nsep,
                     uint8_t* values) {
-  if (orc_num_tokens(n_values, bpv, bpg) != n_tokens) return -1;
+  if (orc_num_tokens(n_values, bpv, bpg, nsep) != n_tokens) return -1;
   int64_t t = 0, byte_no = 0, nbytes = n_values * (int64_t)bpv;
   for (int64_t i = 0; i < n_values; i++) {
     for (int32_t k = 0; k < bpv; k++) {
@@ -102,6 +106,7 @@ int orc_deserialize(const uint8_t* sym, int64_t n_tokens, int64_t n_values,
       byte_no++;
       if (bpg > 0 && (byte_no % bpg == 0 || byte_no == nbytes)) {
         if (sym[t++] != 16) return -1;
+        if (nsep == 2 && sym[t++] != 17) return -1;
       }
     }
   }
@@ -125,13 +130,13 @@ int64_t orc_hex_roundtrip_range(uint64_t lo, uint64_t hi, int32_t msb_first) {
   for (uint64_t base = lo; base < hi; base += BLK) {
     int64_t n = (int64_t)((hi - base) < BLK ? (hi - base) : BLK);
     for (int64_t i = 0; i < n; i++) in[i] = (uint32_t)(base + i);
-    int64_t nt = orc_serialize((const uint8_t*)in, n, 4, 4, msb_first, ids, 32, tok, sym);
+    int64_t nt = orc_serialize((const uint8_t*)in, n, 4, 4, msb_first, ids, 32, -1, tok, sym);
     for (int64_t t = 0; t < nt; t++) {
       int s = sym[t];
       int want = s < 16 ? ids[s] : 32;
       if (tok[t] != want) bad++;
     }
-    if (orc_deserialize(sym, nt, n, 4, 4, msb_first, (uint8_t*)out) != 0) {
+    if (orc_deserialize(sym, nt, n, 4, 4, msb_first, 1, (uint8_t*)out) != 0) {
       bad += n;
       continue;
     }
@@ -146,33 +151,35 @@ int64_t orc_hex_roundtrip_range(uint64_t lo, uint64_t hi, int32_t msb_first) {
 /* ------------------------------------------------------------------------ */
 
 /*
- * lp[17]: float32 natural-log probabilities of the 16 digits and the
- * separator.  cdf[19]: cdf[0] = 0, cdf[k+1] = cdf[k] + f_k, cdf[18] = total.
+ * lp[na]: float32 natural-log probabilities of the na alphabet symbols (16
+ * digits and the separator token(s)); escape bin na takes the rest.
+ * cdf[na+2]: cdf[0] = 0, cdf[k+1] = cdf[k] + f_k, cdf[na+1] = total.
  */
-void orc_quantize(const float* lp, uint32_t total, uint32_t* cdf) {
-  uint32_t f[ORC_NSYM];
+void orc_quantize(const float* lp, int32_t na, uint32_t total, uint32_t* cdf) {
+  uint32_t f[ORC_NSYM_MAX];
+  const int32_t nsym = na + 1;
   uint64_t s = 0;
-  for (int a = 0; a < ORC_NALPHA; a++) {
+  for (int a = 0; a < na; a++) {
     double p = exp((double)lp[a]);
-    double q = floor(p * (double)(total - ORC_NSYM));
+    double q = floor(p * (double)(total - nsym));
     f[a] = 1u + (uint32_t)q;
     s += f[a];
   }
   if (s > (uint64_t)(total - 1)) {
     int big = 0;
-    for (int a = 1; a < ORC_NALPHA; a++)
+    for (int a = 1; a < na; a++)
       if (f[a] > f[big]) big = a;
     f[big] -= (uint32_t)(s - (total - 1));
     s = total - 1;
   }
-  f[ORC_NALPHA] = total - (uint32_t)s;
+  f[na] = total - (uint32_t)s;
   cdf[0] = 0;
-  for (int k = 0; k < ORC_NSYM; k++) cdf[k + 1] = cdf[k] + f[k];
+  for (int k = 0; k < nsym; k++) cdf[k + 1] = cdf[k] + f[k];
 }
 
-void orc_quantize_rows(const float* lp, int64_t rows, uint32_t total, uint32_t* cdf) {
+void orc_quantize_rows(const float* lp, int64_t rows, int32_t na, uint32_t total, uint32_t* cdf) {
   for (int64_t r = 0; r < rows; r++)
-    orc_quantize(lp + r * ORC_NALPHA, total, cdf + r * (ORC_NSYM + 1));
+    orc_quantize(lp + r * na, na, total, cdf + r * (na + 2));
 }
 
 /* ------------------------------------------------------------------------ */

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "coder.c")
 _LIB_PATH = os.path.join(_HERE, "_coder.so")
 
-NALPHA = 17
+NALPHA = 17  # alphabet with a one-token separator (18 with two)
 NSYM = 18
 
 _lib = None
@@ -41,15 +41,15 @@ def lib():
         i64, i32, u32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64
         vp = ctypes.c_void_p
         L.orc_num_tokens.restype = i64
-        L.orc_num_tokens.argtypes = [i64, i32, i32]
+        L.orc_num_tokens.argtypes = [i64, i32, i32, i32]
         L.orc_serialize.restype = i64
-        L.orc_serialize.argtypes = [vp, i64, i32, i32, i32, vp, i32, vp, vp]
+        L.orc_serialize.argtypes = [vp, i64, i32, i32, i32, vp, i32, i32, vp, vp]
         L.orc_deserialize.restype = ctypes.c_int
-        L.orc_deserialize.argtypes = [vp, i64, i64, i32, i32, i32, vp]
+        L.orc_deserialize.argtypes = [vp, i64, i64, i32, i32, i32, i32, vp]
         L.orc_hex_roundtrip_range.restype = i64
         L.orc_hex_roundtrip_range.argtypes = [u64, u64, i32]
         L.orc_quantize_rows.restype = None
-        L.orc_quantize_rows.argtypes = [vp, i64, u32, vp]
+        L.orc_quantize_rows.argtypes = [vp, i64, i32, u32, vp]
         L.orc_ac_encode.restype = i64
         L.orc_ac_encode.argtypes = [vp, i32, vp, i64, vp, u64]
         L.orc_decoder_size.restype = ctypes.c_size_t
@@ -68,34 +68,35 @@ def _p(a: np.ndarray):
 
 
 # ------------------------------------------------------------ serialisation --
-def num_tokens(n_values: int, bytes_per_value: int, bytes_per_group: int) -> int:
-    return int(lib().orc_num_tokens(n_values, bytes_per_value, bytes_per_group))
+def num_tokens(n_values: int, bytes_per_value: int, bytes_per_group: int, nsep: int = 1) -> int:
+    return int(lib().orc_num_tokens(n_values, bytes_per_value, bytes_per_group, nsep))
 
 
 def serialize(values: np.ndarray, bytes_per_value: int, bytes_per_group: int,
-              msb_first: int, hex_ids, sep_id: int):
-    """values: float32 (bpv=4) or uint8 (bpv=1) vector -> (tokens int32, bins uint8)."""
+              msb_first: int, hex_ids, sep_id: int, sep2_id: int = -1):
+    """values: float32 (bpv=4) or uint8 (bpv=1) vector -> (tokens int32, bins uint8).
+    sep2_id >= 0 adds a second separator token (bin 17) after each group."""
     v = np.ascontiguousarray(values)
     assert v.dtype.itemsize == bytes_per_value
     n = v.size
-    nt = num_tokens(n, bytes_per_value, bytes_per_group)
+    nt = num_tokens(n, bytes_per_value, bytes_per_group, 2 if sep2_id >= 0 else 1)
     tok = np.empty(nt, np.int32)
     sym = np.empty(nt, np.uint8)
     ids = np.ascontiguousarray(hex_ids, dtype=np.int32)
     assert ids.size == 16
     got = lib().orc_serialize(_p(v), n, bytes_per_value, bytes_per_group,
-                              msb_first, _p(ids), sep_id, _p(tok), _p(sym))
+                              msb_first, _p(ids), sep_id, sep2_id, _p(tok), _p(sym))
     assert got == nt
     return tok, sym
 
 
 def deserialize(sym: np.ndarray, n_values: int, bytes_per_value: int,
-                bytes_per_group: int, msb_first: int, dtype) -> np.ndarray:
+                bytes_per_group: int, msb_first: int, dtype, nsep: int = 1) -> np.ndarray:
     """Inverse on coder bins; raises ValueError on a malformed stream."""
     s = np.ascontiguousarray(sym, dtype=np.uint8)
     out = np.empty(n_values * bytes_per_value, np.uint8)
     rc = lib().orc_deserialize(_p(s), s.size, n_values, bytes_per_value,
-                               bytes_per_group, msb_first, _p(out))
+                               bytes_per_group, msb_first, nsep, _p(out))
     if rc != 0:
         raise ValueError("malformed token stream")
     return out.view(dtype)
@@ -117,12 +118,14 @@ def hex_roundtrip_all(msb_first: int = 1, threads: int = None) -> int:
 
 # -------------------------------------------------------------- quantiser --
 def quantize(lp: np.ndarray, total: int = 1 << 16) -> np.ndarray:
-    """lp [..., 17] float32 log-probs -> cdf [..., 19] uint32."""
+    """lp [..., A] float32 log-probs of the A alphabet symbols (17, or 18 with
+    a two-token separator) -> cdf [..., A + 2] uint32."""
     a = np.ascontiguousarray(lp, dtype=np.float32)
-    assert a.shape[-1] == NALPHA
-    rows = a.size // NALPHA
-    out = np.empty(a.shape[:-1] + (NSYM + 1,), np.uint32)
-    lib().orc_quantize_rows(_p(a), rows, total, _p(out))
+    na = a.shape[-1]
+    assert na in (17, 18)
+    rows = a.size // na
+    out = np.empty(a.shape[:-1] + (na + 2,), np.uint32)
+    lib().orc_quantize_rows(_p(a), rows, na, total, _p(out))
     return out
 
 

@@ -1,7 +1,7 @@
 """Reference LM-GC codec -- TEST INFRASTRUCTURE ONLY.
 
 Serialise -> cut into windows -> per window: BOS-shifted model input,
-per-position log-probabilities of the 17 alphabet symbols, integer tables,
+per-position log-probabilities of the alphabet symbols, integer tables,
 arithmetic coding -> container.  Decompression mirrors it token by token
 (Sec. 4, "Compression").
 
@@ -25,14 +25,22 @@ HEADER_BYTES = 128
 DEFAULT_TOTAL = 1 << 16
 
 
+def _sep2(serial) -> int:
+    return int(getattr(serial, "sep2_id", -1))
+
+
 def alphabet_ids(serial) -> List[int]:
-    """Token ids of coder bins 0..16: the 16 hex digits, then the separator."""
-    return list(serial.hex_ids) + [serial.sep_id]
+    """Token ids of the coder bins before the escape: the 16 hex digits, the
+    separator, and the second separator token if there is one (H_c+s)."""
+    ids = list(serial.hex_ids) + [serial.sep_id]
+    if _sep2(serial) >= 0:
+        ids.append(_sep2(serial))
+    return ids
 
 
 def serialize(values: np.ndarray, serial):
     return coder.serialize(values, serial.bytes_per_value, serial.bytes_per_group,
-                           serial.msb_first, serial.hex_ids, serial.sep_id)
+                           serial.msb_first, serial.hex_ids, serial.sep_id, _sep2(serial))
 
 
 def windows(n_tokens: int, W: int) -> List[Tuple[int, int]]:
@@ -52,7 +60,7 @@ def model_input(tok_window: np.ndarray, serial, length: int = None) -> np.ndarra
 
 
 def window_logprobs(model: Model, tok_window: np.ndarray, serial, n_pos: int = None) -> np.ndarray:
-    """[n_pos, 17] log-probs of the alphabet at positions 0..n_pos-1."""
+    """[n_pos, A] log-probs of the alphabet at positions 0..n_pos-1."""
     n = tok_window.size if n_pos is None else n_pos
     return model.alphabet_logprobs(model_input(tok_window, serial, n), alphabet_ids(serial))
 
@@ -60,11 +68,12 @@ def window_logprobs(model: Model, tok_window: np.ndarray, serial, n_pos: int = N
 # ---------------------------------------------------------------- container --
 def pack_container(serial, n_values: int, model_tag: int, total: int,
                    bits: List[int], payloads: List[bytes]) -> bytes:
+    nsym = len(alphabet_ids(serial)) + 1
     hdr = struct.pack("<4sHHQQBBBBIII", MAGIC, VERSION, HEADER_BYTES, model_tag,
                       n_values, serial.bytes_per_value, serial.bytes_per_group,
-                      serial.msb_first, coder.NSYM, serial.window, total, len(bits))
-    hdr += struct.pack("<iii16i", serial.bos_id, serial.pad_id, serial.sep_id,
-                       *serial.hex_ids)
+                      serial.msb_first, nsym, serial.window, total, len(bits))
+    hdr += struct.pack("<iii16iI", serial.bos_id, serial.pad_id, serial.sep_id,
+                       *serial.hex_ids, _sep2(serial) + 1)
     hdr += b"\0" * (HEADER_BYTES - len(hdr))
     assert len(hdr) == HEADER_BYTES
     return hdr + struct.pack(f"<{len(bits)}I", *bits) + b"".join(payloads)
@@ -75,9 +84,10 @@ def unpack_container(buf: bytes):
         raise ValueError("not an LM-GC container")
     (magic, ver, hbytes, tag, n_values, bpv, bpg, msb, nsym, W, total,
      nwin) = struct.unpack_from("<4sHHQQBBBBIII", buf, 0)
-    if ver != VERSION or hbytes != HEADER_BYTES or nsym != coder.NSYM:
+    ids = struct.unpack_from("<iii16iI", buf, 40)
+    sep2 = ids[19] - 1
+    if ver != VERSION or hbytes != HEADER_BYTES or nsym != (19 if sep2 >= 0 else 18):
         raise ValueError("unsupported container")
-    ids = struct.unpack_from("<iii16i", buf, 40)
     off = HEADER_BYTES
     if len(buf) < off + 4 * nwin:
         raise ValueError("truncated container")
@@ -92,7 +102,7 @@ def unpack_container(buf: bytes):
         off += nb
     meta = dict(model_tag=tag, n_values=n_values, bytes_per_value=bpv,
                 bytes_per_group=bpg, msb_first=msb, window=W, total=total,
-                bos_id=ids[0], pad_id=ids[1], sep_id=ids[2], hex_ids=ids[3:])
+                bos_id=ids[0], pad_id=ids[1], sep_id=ids[2], hex_ids=ids[3:19], sep2_id=sep2)
     return meta, bits, payloads
 
 
@@ -147,7 +157,8 @@ def decompress(buf: bytes, serial, model: Model, dtype) -> np.ndarray:
     total = meta["total"]
     W = meta["window"]
     n_values = meta["n_values"]
-    n_tokens = coder.num_tokens(n_values, meta["bytes_per_value"], meta["bytes_per_group"])
+    nsep = 2 if meta["sep2_id"] >= 0 else 1
+    n_tokens = coder.num_tokens(n_values, meta["bytes_per_value"], meta["bytes_per_group"], nsep)
     wins = windows(n_tokens, W)
     if len(wins) != len(bits):
         raise ValueError("window count mismatch")
@@ -166,10 +177,10 @@ def decompress(buf: bytes, serial, model: Model, dtype) -> np.ndarray:
         for w, (s, n) in enumerate(wins):
             if j < n:
                 b = decs[w].decode(cdf[w])
-                if b >= coder.NALPHA:
+                if b >= len(ids):
                     raise ValueError("escape symbol decoded: corrupt stream")
                 sym[s + j] = b
                 nxt[w] = id_of[b]
         x = nxt
     return coder.deserialize(sym, n_values, meta["bytes_per_value"],
-                             meta["bytes_per_group"], meta["msb_first"], dtype)
+                             meta["bytes_per_group"], meta["msb_first"], dtype, nsep)

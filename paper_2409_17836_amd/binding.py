@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_HERE, "liblmgc.so")
 LMGC_OK = 0
 ERRORS = {-1: "EINVAL", -2: "ENOMEM", -3: "EDEVICE", -4: "ESIZE", -5: "ECORRUPT",
           -6: "EUNSUPPORTED"}
-NALPHA, NSYM = 17, 18
+NALPHA, NSYM = 17, 18          # with one separator token (A = 17 + escape)
 HEADER_BYTES = 128
 
 KINDS = ["embed", "norm", "gemm_qkv", "attn", "gemm_o", "gemm_up", "gemm_down", "gemm_head",
@@ -34,7 +34,8 @@ class SerialParams(ctypes.Structure):
     _fields_ = [("bytes_per_value", ctypes.c_int32), ("bytes_per_group", ctypes.c_int32),
                 ("msb_first", ctypes.c_int32), ("window", ctypes.c_int32),
                 ("bos_id", ctypes.c_int32), ("pad_id", ctypes.c_int32),
-                ("sep_id", ctypes.c_int32), ("hex_ids", ctypes.c_int32 * 16)]
+                ("sep_id", ctypes.c_int32), ("hex_ids", ctypes.c_int32 * 16),
+                ("sep2_id", ctypes.c_int32)]
 
 
 class ModelConfig(ctypes.Structure):
@@ -68,6 +69,7 @@ def lib():
     sig = {
         "lmgc_last_error": (ctypes.c_char_p, []),
         "lmgc_version": (ctypes.c_char_p, []),
+        "lmgc_alphabet_size": (i32, [P(SerialParams)]),
         "lmgc_num_tokens": (i64, [i64, P(SerialParams)]),
         "lmgc_num_windows": (i64, [i64, P(SerialParams)]),
         "lmgc_serialize": (ctypes.c_int, [vp, i64, P(SerialParams), i64, i64, vp, vp, vp]),
@@ -138,9 +140,19 @@ def serial_params(spec) -> SerialParams:
             ids = list(spec.hex_ids)
             assert len(ids) == 16
             p.hex_ids = (ctypes.c_int32 * 16)(*ids)
+        elif f == "sep2_id":
+            p.sep2_id = int(getattr(spec, "sep2_id", -1))
         else:
             setattr(p, f, int(getattr(spec, f)))
     return p
+
+
+def alphabet_size(sp: SerialParams) -> int:
+    """Coded alphabet size A (17, or 18 with a second separator token)."""
+    n = int(lib().lmgc_alphabet_size(ctypes.byref(sp)))
+    if n < 0:
+        raise LMGCError(-1, lib().lmgc_last_error().decode())
+    return n
 
 
 def model_config(shape) -> ModelConfig:
@@ -253,17 +265,19 @@ def workspace(nbytes: int, device="cuda"):
 
 def probs(model: Model, tokens, sp: SerialParams, total: int = 1 << 16, want_logp: bool = True,
           ws=None, cdf=None, logp=None, stream=None):
-    """tokens: CUDA int32 [B, W] -> (cdf int32 [B, W, 19] holding uint32 values, logp float32 [B, W, 17])."""
+    """tokens: CUDA int32 [B, W] -> (cdf int32 [B, W, A + 2] holding uint32 values,
+    logp float32 [B, W, A]) with A = alphabet_size(sp)."""
     import torch
     B, W = tokens.shape
     assert tokens.dtype == torch.int32 and tokens.is_contiguous()
+    na = alphabet_size(sp)
     need = model.probs_workspace(B, W)
     if ws is None:
         ws = workspace(need, tokens.device)
     if cdf is None:
-        cdf = torch.empty((B, W, NSYM + 1), dtype=torch.int32, device=tokens.device)
+        cdf = torch.empty((B, W, na + 2), dtype=torch.int32, device=tokens.device)
     if logp is None and want_logp:
-        logp = torch.empty((B, W, NALPHA), dtype=torch.float32, device=tokens.device)
+        logp = torch.empty((B, W, na), dtype=torch.float32, device=tokens.device)
     _check(lib().lmgc_probs(model.handle, _ptr(tokens), B, W, ctypes.byref(sp), total, _ptr(cdf),
                             _ptr(logp), _ptr(ws), ws.numel(), _stream(stream)))
     return cdf, logp
@@ -276,10 +290,11 @@ def probs_stepwise(model: Model, tokens, sp: SerialParams, total: int = 1 << 16,
     import torch
     B, W = tokens.shape
     assert tokens.dtype == torch.int32 and tokens.is_contiguous()
+    na = alphabet_size(sp)
     if ws is None:
         ws = workspace(model.step_workspace(B, W), tokens.device)
-    cdf = torch.empty((B, W, NSYM + 1), dtype=torch.int32, device=tokens.device)
-    logp = torch.empty((B, W, NALPHA), dtype=torch.float32, device=tokens.device) if want_logp else None
+    cdf = torch.empty((B, W, na + 2), dtype=torch.int32, device=tokens.device)
+    logp = torch.empty((B, W, na), dtype=torch.float32, device=tokens.device) if want_logp else None
     _check(lib().lmgc_probs_stepwise(model.handle, _ptr(tokens), B, W, ctypes.byref(sp), total,
                                      _ptr(cdf), _ptr(logp), _ptr(ws), ws.numel(), _stream(stream)))
     return cdf, logp

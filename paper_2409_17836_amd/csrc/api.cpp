@@ -41,6 +41,18 @@ static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 static int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
 // ------------------------------------------------------------ serial params
+// Token ids of the coder's alphabet bins (hex digits, then the separator
+// tokens); returns the alphabet size (17 or 18).
+static int alphabet(const lmgc_serial_params& p, int32_t* ids) {
+  for (int i = 0; i < 16; i++) ids[i] = p.hex_ids[i];
+  ids[16] = p.sep_id;
+  if (p.sep2_id >= 0) {
+    ids[17] = p.sep2_id;
+    return 18;
+  }
+  return 17;
+}
+
 static int check_serial(const lmgc_serial_params* p, int vocab) {
   if (!p) return set_error(LMGC_EINVAL, "serial params are NULL");
   if (p->bytes_per_value != 1 && p->bytes_per_value != 2 && p->bytes_per_value != 4)
@@ -49,13 +61,18 @@ static int check_serial(const lmgc_serial_params* p, int vocab) {
     return set_error(LMGC_EINVAL, "bytes_per_group must be in [0, 255]");
   if (p->msb_first != 0 && p->msb_first != 1) return set_error(LMGC_EINVAL, "msb_first must be 0 or 1");
   if (p->window <= 0) return set_error(LMGC_EINVAL, "window must be positive");
+  if (p->sep2_id < -1) return set_error(LMGC_EINVAL, "sep2_id must be -1 (none) or a token id");
+  int32_t ids[LMGC_NALPHA_MAX];
+  const int na = alphabet(*p, ids);
+  for (int a = 0; a < na; a++)
+    for (int b2 = a + 1; b2 < na; b2++)
+      if (ids[a] == ids[b2]) return set_error(LMGC_EINVAL, "alphabet token ids must be distinct (id %d twice)", ids[a]);
   if (vocab > 0) {
-    const int32_t ids[3] = {p->bos_id, p->pad_id, p->sep_id};
-    for (int i = 0; i < 3; i++)
-      if (ids[i] < 0 || ids[i] >= vocab) return set_error(LMGC_EINVAL, "token id %d outside the vocabulary", ids[i]);
-    for (int i = 0; i < 16; i++)
-      if (p->hex_ids[i] < 0 || p->hex_ids[i] >= vocab)
-        return set_error(LMGC_EINVAL, "hex id %d outside the vocabulary", p->hex_ids[i]);
+    const int32_t ext[2] = {p->bos_id, p->pad_id};
+    for (int i = 0; i < 2; i++)
+      if (ext[i] < 0 || ext[i] >= vocab) return set_error(LMGC_EINVAL, "token id %d outside the vocabulary", ext[i]);
+    for (int a = 0; a < na; a++)
+      if (ids[a] < 0 || ids[a] >= vocab) return set_error(LMGC_EINVAL, "alphabet id %d outside the vocabulary", ids[a]);
   }
   return LMGC_OK;
 }
@@ -514,10 +531,9 @@ static int forward(const lmgc_model* m, const int32_t* tok, int B, int W, int dp
   }
   {
     ScopedTimer t(LMGC_K_LSE_CDF, s);
-    int32_t ids[LMGC_NALPHA];
-    for (int i = 0; i < 16; i++) ids[i] = p->hex_ids[i];
-    ids[16] = p->sep_id;
-    HIP_OK(launch_lse_cdf(f.logits, M, m->v_pad, c.vocab, ids, total, cdf, logp, s));
+    int32_t ids[LMGC_NALPHA_MAX];
+    const int na = alphabet(*p, ids);
+    HIP_OK(launch_lse_cdf(f.logits, M, m->v_pad, c.vocab, ids, na, total, cdf, logp, s));
   }
   return LMGC_OK;
 }
@@ -532,7 +548,7 @@ static int run_probs(const lmgc_model* m, const int32_t* tok, int B, int W, cons
   if (W > c.max_pos) return set_error(LMGC_EINVAL, "W=%d exceeds the model's max_pos=%d", W, c.max_pos);
   if (c.dtype == LMGC_DTYPE_BF16 && W % 8) return set_error(LMGC_EUNSUPPORTED, "bf16 models need W %% 8 == 0");
   if ((int64_t)B * W > (1 << 26)) return set_error(LMGC_EUNSUPPORTED, "B*W above 2^26 rows");
-  if (total < 2 * LMGC_NSYM || total > (1u << 24)) return set_error(LMGC_EINVAL, "total must be in [36, 2^24]");
+  if (total < 2 * LMGC_NSYM_MAX || total > (1u << 24)) return set_error(LMGC_EINVAL, "total must be in [38, 2^24]");
   if (!tok || !cdf || !ws) return set_error(LMGC_EINVAL, "NULL device buffer");
   ProbsWs w = carve(m, B, W, (char*)ws);
   if (ws_bytes < w.bytes) return set_error(LMGC_ESIZE, "workspace too small: %zu < %zu", ws_bytes, w.bytes);
@@ -569,8 +585,8 @@ struct StepWs {
   void *a, *q, *o, *ff;
   float* logits;
   int32_t* tok;     // [B] input token of the step (the previous position's)
-  uint32_t* cdf;    // [B, 19]
-  float* logp;      // [B, 17]
+  uint32_t* cdf;    // [B, A + 2] (A: alphabet size)
+  float* logp;      // [B, A]
   char* zero_from;  // q and the caches: cleared for every window group
   size_t zero_bytes, bytes;
   std::vector<void*> kc, vc;
@@ -592,8 +608,8 @@ static StepWs carve_step(const lmgc_model* m, int B, int W, char* base) {
   w.ff = take((size_t)B * c.d_ff * act);
   w.logits = (float*)take((size_t)B * m->v_pad * 4);
   w.tok = (int32_t*)take((size_t)B * 4);
-  w.cdf = (uint32_t*)take((size_t)B * (LMGC_NSYM + 1) * 4);
-  w.logp = (float*)take((size_t)B * LMGC_NALPHA * 4);
+  w.cdf = (uint32_t*)take((size_t)B * (LMGC_NSYM_MAX + 1) * 4);
+  w.logp = (float*)take((size_t)B * LMGC_NALPHA_MAX * 4);
   const size_t z0 = off;
   w.q = take((size_t)B * W * hq * act);
   for (int l = 0; l < c.n_layers; l++) {
@@ -613,7 +629,7 @@ static int check_step(const lmgc_model* m, int B, int W, const lmgc_serial_param
   if (B <= 0 || B > kStepMaxB || W <= 0) return set_error(LMGC_EINVAL, "need 0 < B <= %d and W > 0", kStepMaxB);
   if (W > m->cfg.max_pos) return set_error(LMGC_EINVAL, "W=%d exceeds the model's max_pos=%d", W, m->cfg.max_pos);
   if (m->cfg.dtype == LMGC_DTYPE_BF16 && W % 8) return set_error(LMGC_EUNSUPPORTED, "bf16 models need W %% 8 == 0");
-  if (total < 2 * LMGC_NSYM || total > (1u << 24)) return set_error(LMGC_EINVAL, "total must be in [36, 2^24]");
+  if (total < 2 * LMGC_NSYM_MAX || total > (1u << 24)) return set_error(LMGC_EINVAL, "total must be in [38, 2^24]");
   return LMGC_OK;
 }
 
@@ -634,15 +650,17 @@ static int run_stepwise(const lmgc_model* m, const int32_t* tok, int B, int W, c
   if (!tok || !cdf || !ws) return set_error(LMGC_EINVAL, "NULL device buffer");
   StepWs w = carve_step(m, B, W, (char*)ws);
   if (ws_bytes < w.bytes) return set_error(LMGC_ESIZE, "workspace too small: %zu < %zu", ws_bytes, w.bytes);
+  int32_t ids[LMGC_NALPHA_MAX];
+  const size_t na = alphabet(*p, ids), tw = na + 2;  // alphabet, table width
   HIP_OK(hipMemsetAsync(w.zero_from, 0, w.zero_bytes, s));
   for (int j = 0; j < W; j++) {
     if (j > 0) HIP_OK(hipMemcpy2DAsync(w.tok, 4, tok + (j - 1), (size_t)W * 4, 4, B, hipMemcpyDeviceToDevice, s));
     if ((rc = run_step(m, w, B, W, j, p, total, logp != nullptr, s))) return rc;
-    HIP_OK(hipMemcpy2DAsync(cdf + (size_t)j * (LMGC_NSYM + 1), (size_t)W * (LMGC_NSYM + 1) * 4, w.cdf,
-                            (LMGC_NSYM + 1) * 4, (LMGC_NSYM + 1) * 4, B, hipMemcpyDeviceToDevice, s));
+    HIP_OK(hipMemcpy2DAsync(cdf + (size_t)j * tw, (size_t)W * tw * 4, w.cdf, tw * 4, tw * 4, B,
+                            hipMemcpyDeviceToDevice, s));
     if (logp)
-      HIP_OK(hipMemcpy2DAsync(logp + (size_t)j * LMGC_NALPHA, (size_t)W * LMGC_NALPHA * 4, w.logp, LMGC_NALPHA * 4,
-                              LMGC_NALPHA * 4, B, hipMemcpyDeviceToDevice, s));
+      HIP_OK(hipMemcpy2DAsync(logp + (size_t)j * na, (size_t)W * na * 4, w.logp, na * 4, na * 4, B,
+                              hipMemcpyDeviceToDevice, s));
   }
   return LMGC_OK;
 }
@@ -666,7 +684,7 @@ static CodecWs carve_codec(const lmgc_model* m, int B, int W, char* base) {
   const size_t M = (size_t)B * W;
   c.tok = (int32_t*)take(M * 4);
   c.sym = (uint8_t*)take(M);
-  c.cdf = (uint32_t*)take(M * (LMGC_NSYM + 1) * 4);
+  c.cdf = (uint32_t*)take(M * (LMGC_NSYM_MAX + 1) * 4);
   c.probs_bytes = carve(m, B, W, nullptr).bytes;
   c.probs = take(c.probs_bytes);
   c.bytes = off;
@@ -701,9 +719,11 @@ static int compress(const lmgc_model* m, const void* d_values, int64_t n_values,
   if (cap < head_bytes) return set_error(LMGC_ESIZE, "output buffer too small for the header");
 
   const size_t M = (size_t)B * W;
+  int32_t alpha_ids[LMGC_NALPHA_MAX];
+  const int nsym = alphabet(*p, alpha_ids) + 1;  // coder bins incl. escape
   PinnedBuf hc[2], hs[2];
   for (int i = 0; i < 2; i++) {
-    HIP_OK(hipHostMalloc(&hc[i].p, M * (LMGC_NSYM + 1) * 4, hipHostMallocDefault));
+    HIP_OK(hipHostMalloc(&hc[i].p, M * (nsym + 1) * 4, hipHostMallocDefault));
     HIP_OK(hipHostMalloc(&hs[i].p, M, hipHostMallocDefault));
   }
   hipEvent_t ev[2];
@@ -732,7 +752,7 @@ static int compress(const lmgc_model* m, const void* d_values, int64_t n_values,
       lens[i] = (int)std::min<int64_t>(W, nt - gw * W);
     }
     size_t u = 0;
-    int r = encode_windows((const uint32_t*)hc[b & 1].p, LMGC_NSYM, (const uint8_t*)hs[b & 1].p, lens.data(), nb, W,
+    int r = encode_windows((const uint32_t*)hc[b & 1].p, nsym, (const uint8_t*)hs[b & 1].p, lens.data(), nb, W,
                            out + pos, cap - pos, bits.data() + w0, &u, 0);
     if (r) return r;
     pos += u;
@@ -744,7 +764,7 @@ static int compress(const lmgc_model* m, const void* d_values, int64_t n_values,
     HIP_OK(launch_serialize(d_values, n_values, *p, first_window + w0, nb, cw.tok, cw.sym, s));
     rc = run_probs(m, cw.tok, nb, W, p, total, cw.cdf, nullptr, cw.probs, cw.probs_bytes, s);
     if (rc) return rc;
-    HIP_OK(hipMemcpyAsync(hc[b & 1].p, cw.cdf, (size_t)nb * W * (LMGC_NSYM + 1) * 4, hipMemcpyDeviceToHost, s));
+    HIP_OK(hipMemcpyAsync(hc[b & 1].p, cw.cdf, (size_t)nb * W * (nsym + 1) * 4, hipMemcpyDeviceToHost, s));
     HIP_OK(hipMemcpyAsync(hs[b & 1].p, cw.sym, (size_t)nb * W, hipMemcpyDeviceToHost, s));
     HIP_OK(hipEventRecord(ev[b & 1], s));
     if (b > 0) {
@@ -791,10 +811,9 @@ static int decode(const lmgc_model* m, const uint8_t* buf, size_t bytes, int32_t
   if (off[h.n_windows] > bytes) return set_error(LMGC_ECORRUPT, "container: truncated payload");
 
   std::vector<uint8_t> sym((size_t)std::max<int64_t>(nt, 1));
-  std::vector<int32_t> id_of(LMGC_NALPHA);
-  for (int i = 0; i < 16; i++) id_of[i] = h.p.hex_ids[i];
-  id_of[16] = h.p.sep_id;
-  std::vector<uint32_t> rows((size_t)G * (LMGC_NSYM + 1));
+  std::vector<int32_t> id_of(LMGC_NALPHA_MAX);
+  const int na = alphabet(h.p, id_of.data()), nsym = na + 1;
+  std::vector<uint32_t> rows((size_t)G * (nsym + 1));
   std::vector<int32_t> col(G);
   std::vector<lmgc_decoder> dec(G);
   // Window groups, token by token from BOS: one decoding step gives every
@@ -812,14 +831,14 @@ static int decode(const lmgc_model* m, const uint8_t* buf, size_t bytes, int32_t
     HIP_OK(hipMemsetAsync(sw.zero_from, 0, sw.zero_bytes, s));
     for (int j = 0; j < maxlen; j++) {
       if ((rc = run_step(m, sw, nb, W, j, &h.p, h.total, false, s))) return rc;
-      HIP_OK(hipMemcpyAsync(rows.data(), sw.cdf, (size_t)nb * (LMGC_NSYM + 1) * 4, hipMemcpyDeviceToHost, s));
+      HIP_OK(hipMemcpyAsync(rows.data(), sw.cdf, (size_t)nb * (nsym + 1) * 4, hipMemcpyDeviceToHost, s));
       HIP_OK(hipStreamSynchronize(s));
       for (int i = 0; i < nb; i++) {
         col[i] = h.p.pad_id;
         if (j >= len[i]) continue;
         int32_t b = 0;
-        if ((rc = decoder_symbol(&dec[i], rows.data() + (size_t)i * (LMGC_NSYM + 1), LMGC_NSYM, &b))) return rc;
-        if (b >= LMGC_NALPHA) return set_error(LMGC_ECORRUPT, "escape symbol decoded (window %lld, position %d)",
+        if ((rc = decoder_symbol(&dec[i], rows.data() + (size_t)i * (nsym + 1), nsym, &b))) return rc;
+        if (b >= na) return set_error(LMGC_ECORRUPT, "escape symbol decoded (window %lld, position %d)",
                                               (long long)(w0 + i), j);
         sym[(size_t)(w0 + i) * W + j] = (uint8_t)b;
         col[i] = id_of[b];
@@ -840,6 +859,13 @@ extern "C" {
 
 const char* lmgc_last_error(void) { return g_err; }
 const char* lmgc_version(void) { return "lmgc 0.1 gfx950"; }
+
+int32_t lmgc_alphabet_size(const lmgc_serial_params* p) {
+  clear_error();
+  if (check_serial(p, 0)) return -1;
+  int32_t ids[LMGC_NALPHA_MAX];
+  return alphabet(*p, ids);
+}
 
 int64_t lmgc_num_tokens(int64_t n_values, const lmgc_serial_params* p) {
   if (check_serial(p, 0) || n_values < 0) return -1;

@@ -246,7 +246,7 @@ int decoder_symbol(lmgc_decoder* st, const uint32_t* c, int nsym, int32_t* out) 
 int64_t num_tokens(int64_t n_values, const lmgc_serial_params& p) {
   const int64_t nbytes = n_values * p.bytes_per_value;
   const int64_t groups = p.bytes_per_group > 0 ? (nbytes + p.bytes_per_group - 1) / p.bytes_per_group : 0;
-  return 2 * nbytes + groups;
+  return 2 * nbytes + groups * (p.sep2_id >= 0 ? 2 : 1);
 }
 
 int deserialize_bins(const uint8_t* sym, int64_t n_tokens, int64_t n_values,
@@ -267,6 +267,7 @@ int deserialize_bins(const uint8_t* sym, int64_t n_tokens, int64_t n_values,
     if (bpg > 0 && (++in_group == bpg || byte + 1 == nbytes)) {
       in_group = 0;
       if (sym[t++] != 16) return set_error(LMGC_ECORRUPT, "lmgc_deserialize: separator expected");
+      if (p.sep2_id >= 0 && sym[t++] != 17) return set_error(LMGC_ECORRUPT, "lmgc_deserialize: separator expected");
     }
   }
   return LMGC_OK;
@@ -290,7 +291,7 @@ void write_header(uint8_t* h, const ContainerHeader& c) {
   h[24] = (uint8_t)c.p.bytes_per_value;
   h[25] = (uint8_t)c.p.bytes_per_group;
   h[26] = (uint8_t)c.p.msb_first;
-  h[27] = LMGC_NSYM;
+  h[27] = (uint8_t)(c.p.sep2_id >= 0 ? LMGC_NALPHA_MAX + 1 : LMGC_NALPHA + 1);
   put_u32(h + 28, (uint32_t)c.p.window);
   put_u32(h + 32, c.total);
   put_u32(h + 36, (uint32_t)c.n_windows);
@@ -298,12 +299,13 @@ void write_header(uint8_t* h, const ContainerHeader& c) {
   put_u32(h + 44, (uint32_t)c.p.pad_id);
   put_u32(h + 48, (uint32_t)c.p.sep_id);
   for (int i = 0; i < 16; i++) put_u32(h + 52 + 4 * i, (uint32_t)c.p.hex_ids[i]);
+  put_u32(h + 116, (uint32_t)(c.p.sep2_id + 1));
 }
 
 int read_header(const uint8_t* buf, size_t bytes, ContainerHeader* c) {
   if (bytes < LMGC_HEADER_BYTES || memcmp(buf, "LMGC", 4) != 0)
     return set_error(LMGC_ECORRUPT, "container: bad magic or truncated header");
-  if (get_u16(buf + 4) != 1 || get_u16(buf + 6) != LMGC_HEADER_BYTES || buf[27] != LMGC_NSYM)
+  if (get_u16(buf + 4) != 1 || get_u16(buf + 6) != LMGC_HEADER_BYTES)
     return set_error(LMGC_ECORRUPT, "container: unsupported version");
   c->model_tag = get_u64(buf + 8);
   c->n_values = (int64_t)get_u64(buf + 16);
@@ -317,6 +319,9 @@ int read_header(const uint8_t* buf, size_t bytes, ContainerHeader* c) {
   c->p.pad_id = (int32_t)get_u32(buf + 44);
   c->p.sep_id = (int32_t)get_u32(buf + 48);
   for (int i = 0; i < 16; i++) c->p.hex_ids[i] = (int32_t)get_u32(buf + 52 + 4 * i);
+  c->p.sep2_id = (int32_t)get_u32(buf + 116) - 1;
+  if (buf[27] != (c->p.sep2_id >= 0 ? LMGC_NALPHA_MAX + 1 : LMGC_NALPHA + 1))
+    return set_error(LMGC_ECORRUPT, "container: symbol count does not match the separators");
   if (c->n_values < 0 || c->p.window <= 0 ||
       (c->p.bytes_per_value != 1 && c->p.bytes_per_value != 2 && c->p.bytes_per_value != 4))
     return set_error(LMGC_ECORRUPT, "container: bad header fields");

@@ -96,10 +96,10 @@ hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uin
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,
                                 int B, int Hq, int Hkv, int W, int hd, int dq, hipStream_t s);
 
-// logits [M, ldz] (first V valid) -> cdf [M, 19], logp [M, 17] (nullable);
-// alpha_ids is a host array of the 17 alphabet token ids.
+// logits [M, ldz] (first V valid) -> cdf [M, A + 2], logp [M, A] (nullable);
+// alpha_ids is a host array of the A = n_alpha (17 or 18) alphabet token ids.
 hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
-                          uint32_t total, uint32_t* cdf, float* logp, hipStream_t s);
+                          int n_alpha, uint32_t total, uint32_t* cdf, float* logp, hipStream_t s);
 
 // dst[r, :] = srcs.p[idx[r] >> 28][(idx[r] & 0x0fffffff), :] for r < rows;
 // idx[r] == -1 gives a zero row.  Rows are cols * elem_bytes bytes (multiple of 4).

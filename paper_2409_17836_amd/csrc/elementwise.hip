@@ -13,7 +13,7 @@ namespace {
 constexpr int kWave = 64;
 
 struct AlphaIds {
-  int32_t v[LMGC_NALPHA];
+  int32_t v[LMGC_NALPHA_MAX];
 };
 
 __device__ inline float wave_sum(float v) {
@@ -159,11 +159,14 @@ __global__ void norm_bf16x4_kernel(const float* __restrict__ h, int M, const uin
 }
 
 // ------------------------------------------------------------ LSE + table
-// One wave per row: online max / sum-exp over the V logits, then the 17
-// alphabet log-probabilities and their integer table (quantised in double).
+// One wave per row: online max / sum-exp over the V logits, then the NA
+// alphabet log-probabilities and their integer table of NA + 2 entries
+// (quantised in double; escape bin NA).
+template <int NA>
 __global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int V,
                                AlphaIds ids, uint32_t total,
                                uint32_t* __restrict__ cdf, float* __restrict__ logp) {
+  constexpr int NS = NA + 1;  // coder bins incl. escape
   const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (row >= M) return;
@@ -197,37 +200,37 @@ __global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int 
   const float lse = m + logf(s);
   uint32_t f = 0;
   float lp = 0.f;
-  if (lane < LMGC_NALPHA) {
+  if (lane < NA) {
     lp = zr[ids.v[lane]] - lse;
     const double p = exp((double)lp);
-    f = 1u + (uint32_t)floor(p * (double)(total - LMGC_NSYM));
-    if (logp) logp[row * LMGC_NALPHA + lane] = lp;
+    f = 1u + (uint32_t)floor(p * (double)(total - NS));
+    if (logp) logp[row * NA + lane] = lp;
   }
-  uint32_t fa[LMGC_NALPHA];
+  uint32_t fa[NA];
   uint64_t S = 0;
 #pragma unroll
-  for (int a = 0; a < LMGC_NALPHA; a++) {
+  for (int a = 0; a < NA; a++) {
     fa[a] = (uint32_t)__shfl((int)f, a, kWave);
     S += fa[a];
   }
   if (S > (uint64_t)(total - 1)) {
     int big = 0;
 #pragma unroll
-    for (int a = 1; a < LMGC_NALPHA; a++)
+    for (int a = 1; a < NA; a++)
       if (fa[a] > fa[big]) big = a;
     const uint32_t ex = (uint32_t)(S - (total - 1));
 #pragma unroll
-    for (int a = 0; a < LMGC_NALPHA; a++)
+    for (int a = 0; a < NA; a++)
       if (a == big) fa[a] -= ex;
     S = total - 1;
   }
-  if (lane <= LMGC_NSYM) {
+  if (lane <= NS) {
     uint32_t c = 0;
 #pragma unroll
-    for (int a = 0; a < LMGC_NALPHA; a++)
+    for (int a = 0; a < NA; a++)
       if (a < lane) c += fa[a];
-    if (lane == LMGC_NSYM) c = total;
-    cdf[row * (LMGC_NSYM + 1) + lane] = c;
+    if (lane == NS) c = total;
+    cdf[row * (NS + 1) + lane] = c;
   }
 }
 
@@ -298,11 +301,16 @@ hipError_t launch_norm(const float* h, int M, int d, const void* gain, const voi
 }
 
 hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
-                          uint32_t total, uint32_t* cdf, float* logp, hipStream_t s) {
-  AlphaIds ids;
-  for (int a = 0; a < LMGC_NALPHA; a++) ids.v[a] = alpha_ids[a];
-  hipLaunchKernelGGL(lse_cdf_kernel, dim3((unsigned)((M + 3) / 4)), dim3(256), 0, s, logits, M,
-                     ldz, V, ids, total, cdf, logp);
+                          int n_alpha, uint32_t total, uint32_t* cdf, float* logp, hipStream_t s) {
+  AlphaIds ids = {};
+  if (n_alpha != LMGC_NALPHA && n_alpha != LMGC_NALPHA_MAX) return hipErrorInvalidValue;
+  for (int a = 0; a < n_alpha; a++) ids.v[a] = alpha_ids[a];
+  const dim3 grid((unsigned)((M + 3) / 4)), block(256);
+  if (n_alpha == LMGC_NALPHA)
+    hipLaunchKernelGGL(lse_cdf_kernel<LMGC_NALPHA>, grid, block, 0, s, logits, M, ldz, V, ids, total, cdf, logp);
+  else
+    hipLaunchKernelGGL(lse_cdf_kernel<LMGC_NALPHA_MAX>, grid, block, 0, s, logits, M, ldz, V, ids, total, cdf,
+                       logp);
   return hipGetLastError();
 }
 

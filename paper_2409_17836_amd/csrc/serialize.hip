@@ -2,7 +2,8 @@
 // (Sec. 4, "Serialization").  Each thread produces four consecutive tokens of
 // the window range and stores them with one 16-byte and one 4-byte store;
 // the value bytes it needs are read through the cache (nine tokens share
-// one float32).  The work is HBM-bound: 4/9 B read and 5 B written per token.
+// one float32).  The work is HBM-bound: 4/9 B read and 5 B written per token
+// (one separator token; 4/10 B and 5 B with two).
 #include "common.h"
 
 namespace lmgc {
@@ -11,7 +12,7 @@ namespace {
 struct SerialDev {
   int64_t n_values, n_tokens, nbytes;
   int32_t bpv, bpg, msb_first, W;
-  int32_t pad_id, sep_id;
+  int32_t pad_id, nsep, sep[2];  // separator tokens after each group (bins 16, 17)
   int32_t hex[16];
 };
 
@@ -23,16 +24,16 @@ __device__ inline void token_at(const uint8_t* __restrict__ vals, const SerialDe
     return;
   }
   int64_t byte;
-  int is_sep = 0, low = 0;
+  int sep = -1, low = 0;
   if (p.bpg > 0) {
-    const int64_t G = 2 * (int64_t)p.bpg + 1;
+    const int64_t G = 2 * (int64_t)p.bpg + p.nsep;  // a full group's tokens
     const int64_t g = t / G;
     const int32_t r = (int32_t)(t - g * G);
     const int64_t b0 = g * p.bpg;
     const int64_t left = p.nbytes - b0;
     const int32_t nb = left < p.bpg ? (int32_t)left : p.bpg;
     if (r >= 2 * nb) {
-      is_sep = 1;
+      sep = r - 2 * nb;  // 0 or 1
       byte = 0;
     } else {
       byte = b0 + (r >> 1);
@@ -42,9 +43,9 @@ __device__ inline void token_at(const uint8_t* __restrict__ vals, const SerialDe
     byte = t >> 1;
     low = (int)(t & 1);
   }
-  if (is_sep) {
-    tok = p.sep_id;
-    sym = 16;
+  if (sep >= 0) {
+    tok = p.sep[sep];
+    sym = (uint8_t)(16 + sep);
     return;
   }
   const int64_t i = byte / p.bpv;
@@ -94,11 +95,13 @@ hipError_t launch_serialize(const void* values, int64_t n_values, const lmgc_ser
   p.msb_first = sp.msb_first;
   p.W = sp.window;
   p.pad_id = sp.pad_id;
-  p.sep_id = sp.sep_id;
+  p.nsep = sp.sep2_id >= 0 ? 2 : 1;
+  p.sep[0] = sp.sep_id;
+  p.sep[1] = sp.sep2_id;
   for (int i = 0; i < 16; i++) p.hex[i] = sp.hex_ids[i];
   p.nbytes = n_values * (int64_t)sp.bytes_per_value;
   p.n_tokens = 2 * p.nbytes + (sp.bytes_per_group > 0
-                                   ? (p.nbytes + sp.bytes_per_group - 1) / sp.bytes_per_group
+                                   ? (p.nbytes + sp.bytes_per_group - 1) / sp.bytes_per_group * p.nsep
                                    : 0);
   const int64_t t0 = first_window * sp.window;
   const int64_t n_local = n_windows * sp.window;

@@ -47,18 +47,25 @@ class SerialSpec:
     pad_id: int
     sep_id: int
     hex_ids: Tuple[int, ...] = field(default=tuple(ord(c) for c in HEX_CHARS))
+    sep2_id: int = -1             # second separator token after each group; -1 = none
+
+
+# The separators of the paper's hexadecimal serialisations (Section 5.2,
+# Table 1), as (sep_id, sep2_id) character codes; H_n is bytes_per_group = 0.
+SEPARATORS = {"H_s": (ord(" "), -1), "H_c": (ord(","), -1), "H_semi": (ord(";"), -1),
+              "H_c+s": (ord(","), ord(" "))}
 
 
 def hex_serial(window: int, bos_id: int, bytes_per_value: int = 4,
                bytes_per_group: int = None, msb_first: int = 1,
-               sep_id: int = 32) -> SerialSpec:
-    """H_s serialisation: lowercase hex digits, a space after each group."""
+               sep_id: int = 32, sep2_id: int = -1) -> SerialSpec:
+    """Hexadecimal serialisation (H_s by default: a space after each group)."""
     if bytes_per_group is None:
         bytes_per_group = bytes_per_value
     return SerialSpec(bytes_per_value=bytes_per_value,
                       bytes_per_group=bytes_per_group, msb_first=msb_first,
                       window=window, bos_id=bos_id, pad_id=bos_id,
-                      sep_id=sep_id)
+                      sep_id=sep_id, sep2_id=sep2_id)
 
 
 @dataclass(frozen=True)

@@ -10,7 +10,7 @@ from oracle import pipeline as opipe
 from oracle.forward import Model as OModel
 from paper_2409_17836_amd import binding as B
 from synth import get_workload
-from synth.configs import hex_serial
+from synth.configs import SEPARATORS, hex_serial
 from synth.gen import gen_values, workload_values
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(600)]
@@ -46,6 +46,20 @@ def test_tiny_bytes_per_group_variants():
     vals = gen_values("laplace:1e-3", 150, 8)
     for bpg in (0, 1, 2, 3, 8):
         _roundtrip(model, om, vals, hex_serial(window=256, bos_id=1, bytes_per_group=bpg), batch=4)
+    model.close()
+
+
+def test_tiny_separator_variants():
+    """H_c, H_semi and H_c+s (Sec. 5.2); H_c+s codes 18 alphabet symbols."""
+    w = get_workload("tiny")
+    model, host = build_model(w.model, w.weight_seed)
+    om = OModel(w.model, host)
+    vals = gen_values("laplace:1e-3", 150, 9)
+    for variant, (sep, sep2) in sorted(SEPARATORS.items()):
+        log(f"separator variant {variant}")
+        spec = hex_serial(window=256, bos_id=1, sep_id=sep, sep2_id=sep2)
+        buf = _roundtrip(model, om, vals, spec, batch=4)
+        assert buf[27] == (19 if sep2 >= 0 else 18)
     model.close()
 
 

@@ -60,6 +60,33 @@ def test_tiny_whole_workload_logprobs(which, tiny, tiny_perturbed):
     assert np.array_equal(cdf.cpu().numpy().view(np.uint32), ocoder.quantize(lp))
 
 
+def test_tiny_two_token_separator_tables(tiny_perturbed):
+    """H_c+s: 18 alphabet log-probs and 20-entry tables per position."""
+    import dataclasses
+    import torch
+    w, model, om = tiny_perturbed
+    ser = dataclasses.replace(w.serial, sep_id=44, sep2_id=32)
+    vals = workload_values(w)[:400]                 # 15 windows (stepwise: B <= 16)
+    sp = B.serial_params(ser)
+    nw = B.num_windows(vals.size, sp)
+    tok, _ = B.serialize(torch.from_numpy(vals).cuda(), sp, 0, nw)
+    cdf, logp = B.probs(model, tok, sp)
+    torch.cuda.synchronize()
+    assert tuple(cdf.shape) == (nw, ser.window, 20) and tuple(logp.shape) == (nw, ser.window, 18)
+    lp = logp.cpu().numpy()
+    otok, _ = opipe.serialize(vals, ser)
+    X = np.stack([opipe.model_input(otok[s:s + n], ser, ser.window)
+                  for s, n in opipe.windows(otok.size, ser.window)])
+    ref = om.alphabet_logprobs(X, opipe.alphabet_ids(ser))
+    err = np.abs(lp - ref).max()
+    log(f"tiny H_c+s: max |lp - oracle| = {err:.3g}")
+    assert err <= 1e-4
+    assert np.array_equal(cdf.cpu().numpy().view(np.uint32), ocoder.quantize(lp))
+    cdf2, logp2 = B.probs_stepwise(model, tok, sp)
+    assert np.array_equal(cdf2.cpu().numpy(), cdf.cpu().numpy())
+    assert np.array_equal(logp2.cpu().numpy().view(np.uint32), lp.view(np.uint32))
+
+
 @pytest.fixture(scope="module")
 def gpt2():
     w = get_workload("gpt2")

@@ -1,6 +1,6 @@
 """lmgc_serialize on the GPU vs the oracle's serialiser: bit-exact tokens and
 coder bins, including window ranges, the padded last window, byte orders,
-separator groupings, 8-bit values and the full-size 7B-shape vector."""
+separator groupings and variants, 8-bit values and the full-size 7B-shape vector."""
 import numpy as np
 import pytest
 
@@ -8,7 +8,7 @@ from gpu_util import log
 from oracle import coder as ocoder
 from paper_2409_17836_amd import binding as B
 from synth import get_workload
-from synth.configs import hex_serial
+from synth.configs import SEPARATORS, hex_serial
 from synth.gen import gen_values, workload_values
 
 pytestmark = pytest.mark.gpu
@@ -21,7 +21,7 @@ def _check(vals, spec, first=0, count=None):
     tok, sym = B.serialize(dv, sp, first, count)
     torch.cuda.synchronize()
     otok, osym = ocoder.serialize(vals, spec.bytes_per_value, spec.bytes_per_group, spec.msb_first,
-                                  spec.hex_ids, spec.sep_id)
+                                  spec.hex_ids, spec.sep_id, spec.sep2_id)
     W = spec.window
     nw = tok.shape[0]
     ftok = np.full((first + nw) * W, spec.pad_id, np.int32)
@@ -63,3 +63,17 @@ def test_serialize_window_ranges_and_edges():
     _check(vals[:1], spec)                                 # one value
     special = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 1e-45, -3.4e38], np.float32)
     _check(special, spec)
+
+
+@pytest.mark.parametrize("variant", sorted(SEPARATORS))
+@pytest.mark.parametrize("bpv,bpg", [(4, 4), (4, 3), (1, 1), (2, 8)])
+def test_serialize_separator_variants(variant, bpv, bpg):
+    """Sec. 5.2 separators, H_c+s with two tokens per group (bins 16, 17)."""
+    sep, sep2 = SEPARATORS[variant]
+    n = 777
+    raw = np.random.default_rng(bpg + 10 * bpv).integers(0, 256, n * bpv, dtype=np.uint8)
+    vals = raw.view({1: np.uint8, 2: np.int16, 4: np.float32}[bpv])
+    spec = hex_serial(window=96, bos_id=1, bytes_per_value=bpv, bytes_per_group=bpg,
+                      sep_id=sep, sep2_id=sep2)
+    _check(vals, spec)
+    _check(vals, spec, first=2, count=3)

@@ -112,6 +112,47 @@ def test_library_deserialize_matches_oracle(bpv, bpg, msb):
         assert e.value.code == -5
 
 
+@pytest.mark.parametrize("bpv,bpg,msb", [(4, 4, 1), (4, 4, 0), (4, 3, 1), (1, 1, 1), (2, 8, 1)])
+def test_library_two_token_separator_matches_oracle(bpv, bpg, msb):
+    """H_c+s (Sec. 5.2): token counts, alphabet size and deserialisation."""
+    rng = np.random.default_rng(7 * bpv + bpg + msb)
+    dt = {1: np.uint8, 2: np.uint16, 4: np.float32}[bpv]
+    vals = rng.integers(0, 256, 333 * bpv, dtype=np.uint8).view(dt)
+    hex_ids = list(range(48, 64))
+    _, sym = ocoder.serialize(vals, bpv, bpg, msb, hex_ids, 44, 32)
+    sp = B.serial_params(hex_serial(window=64, bos_id=1, bytes_per_value=bpv, bytes_per_group=bpg,
+                                    msb_first=msb, sep_id=44, sep2_id=32))
+    assert B.alphabet_size(sp) == 18
+    for n in (0, 1, 5, vals.size):
+        assert B.num_tokens(n, sp) == ocoder.num_tokens(n, bpv, bpg, 2)
+    assert B.deserialize(sym, vals.size, sp, dt).tobytes() == vals.tobytes()
+    bad = sym.copy()
+    bad[2 * bpg], bad[2 * bpg + 1] = bad[2 * bpg + 1], bad[2 * bpg]     # ", " -> " ,"
+    with pytest.raises(B.LMGCError) as e:
+        B.deserialize(bad, vals.size, sp, dt)
+    assert e.value.code == -5
+
+
+def test_library_serial_params_validation():
+    assert B.alphabet_size(B.serial_params(hex_serial(window=8, bos_id=1))) == 17
+    for sep, sep2 in ((44, 44), (44, 48), (44, -2), (48, -1)):   # repeats, digit ids, bad id
+        sp = B.serial_params(hex_serial(window=8, bos_id=1, sep_id=sep, sep2_id=sep2))
+        with pytest.raises(B.LMGCError) as e:
+            B.alphabet_size(sp)
+        assert e.value.code == -1
+
+
+def test_library_reads_two_token_separator_container():
+    ser = hex_serial(window=8, bos_id=1, sep_id=44, sep2_id=32)
+    buf = opipe.pack_container(ser, 3, 5, 1 << 16, [7, 9, 1, 2], [b"\x01", b"\x02\x03", b"\x04", b"\x05"])
+    assert buf[27] == 19 and int.from_bytes(buf[116:120], "little") == 33
+    assert B.container_info(buf) == dict(n_values=3, bytes_per_value=4, n_windows=4, model_tag=5)
+    bad = bytearray(buf)
+    bad[27] = 18                     # bin count of a one-token alphabet with a second id
+    with pytest.raises(B.LMGCError):
+        B.container_info(bytes(bad))
+
+
 def test_container_info_and_corruption():
     ser = hex_serial(window=8, bos_id=1)
     bits = [13, 20, 5]

@@ -85,6 +85,79 @@ def test_deserialize_rejects_malformed():
         coder.deserialize(bad, 2, 4, 4, 1, np.float32)
 
 
+# The paper's separator variants (Sec. 5.2, Table 1): H_s (space), H_c (comma),
+# H_semi (semicolon), H_c+s (comma then space: two tokens, coder bins 16 and
+# 17) and H_n (no separator: bytes per group 0).
+@pytest.mark.parametrize("sep,sep2,text", [
+    (ord(" "), -1, "3f800000 c0000000 "),
+    (ord(","), -1, "3f800000,c0000000,"),
+    (ord(";"), -1, "3f800000;c0000000;"),
+    (ord(","), ord(" "), "3f800000, c0000000, "),
+])
+def test_separator_variants_closed_forms(sep, sep2, text):
+    tok, sym = coder.serialize(np.array([1.0, -2.0], np.float32), 4, 4, 1, HEX, sep, sep2)
+    assert _text(tok) == text
+    digits = [int(c, 16) for c in "3f800000"], [int(c, 16) for c in "c0000000"]
+    tail = [16, 17] if sep2 >= 0 else [16]
+    assert list(sym) == digits[0] + tail + digits[1] + tail
+    nsep = 2 if sep2 >= 0 else 1
+    assert coder.num_tokens(2, 4, 4, nsep) == tok.size
+    for n in (0, 1, 7, 1000):
+        assert coder.num_tokens(n, 4, 4, nsep) == (8 + nsep) * n
+
+
+def test_no_separator_variant():
+    tok, sym = coder.serialize(np.array([1.0, -2.0], np.float32), 4, 0, 1, HEX, 32)
+    assert _text(tok) == "3f800000c0000000"
+    assert sym.max() < 16
+
+
+@pytest.mark.parametrize("bpv,bpg", [(4, 1), (4, 2), (4, 3), (4, 4), (4, 8), (1, 1), (2, 3)])
+@pytest.mark.parametrize("msb", [1, 0])
+def test_two_token_separator_structure_and_roundtrip(bpv, bpg, msb):
+    rng = np.random.default_rng(11 * bpg + bpv + msb)
+    n = 29
+    dt = {1: np.uint8, 2: np.uint16, 4: np.float32}[bpv]
+    vals = rng.integers(0, 256, n * bpv, dtype=np.uint8).view(dt)
+    tok, sym = coder.serialize(vals, bpv, bpg, msb, HEX, ord(","), ord(" "))
+    nbytes = n * bpv
+    assert tok.size == 2 * nbytes + 2 * -(-nbytes // bpg)
+    # brute force from Python's hex formatting, ", " closing every group
+    stream = b"".join(v.tobytes()[::-1] if msb else v.tobytes() for v in vals)
+    want = []
+    for i, byte in enumerate(stream):
+        want.append(f"{byte:02x}")
+        if (i + 1) % bpg == 0 or i + 1 == nbytes:
+            want.append(", ")
+    assert _text(tok) == "".join(want)
+    back = coder.deserialize(sym, n, bpv, bpg, msb, dt, nsep=2)
+    assert back.tobytes() == vals.tobytes()
+    # the one-token reading of the same stream is malformed
+    with pytest.raises(ValueError):
+        coder.deserialize(sym, n, bpv, bpg, msb, dt, nsep=1)
+
+
+def test_two_token_separator_rejects_malformed():
+    vals = np.array([1.0, 2.0, 3.0], np.float32)
+    _, sym = coder.serialize(vals, 4, 4, 1, HEX, ord(","), ord(" "))
+    assert list(sym[8:10]) == [16, 17]
+    for i, j in ((8, 9), (7, 8), (9, 10)):        # swapped separator tokens, digit/separator
+        bad = sym.copy()
+        bad[i], bad[j] = bad[j], bad[i]
+        with pytest.raises(ValueError):
+            coder.deserialize(bad, 3, 4, 4, 1, np.float32, nsep=2)
+    bad = sym.copy()
+    bad[19] = 16                                  # first separator token twice
+    with pytest.raises(ValueError):
+        coder.deserialize(bad, 3, 4, 4, 1, np.float32, nsep=2)
+    bad = sym.copy()
+    bad[3] = 18                                   # escape bin in the data
+    with pytest.raises(ValueError):
+        coder.deserialize(bad, 3, 4, 4, 1, np.float32, nsep=2)
+    with pytest.raises(ValueError):
+        coder.deserialize(sym[:-1], 3, 4, 4, 1, np.float32, nsep=2)
+
+
 @pytest.mark.slow
 def test_hex_roundtrip_all_float32_bit_patterns():
     """Every one of the 2^32 patterns (NaN payloads, +-0, subnormals, +-inf)
@@ -114,6 +187,23 @@ def test_quantize_uniform_closed_form(V, f_alpha, f_esc):
     assert (cdf[:, 0] == 0).all() and (cdf[:, -1] == 65536).all()
 
 
+@pytest.mark.parametrize("V,f_alpha,f_esc", [
+    # 18-symbol alphabet (two-token separator): f = 1 + floor((1/V) * 65517),
+    # esc = 65536 - 18 f
+    (256, 256, 60928),
+    (32000, 3, 65482),
+    (50257, 2, 65500),
+])
+def test_quantize_uniform_closed_form_18_symbols(V, f_alpha, f_esc):
+    lp = np.full((2, 18), -math.log(V), np.float32)
+    cdf = coder.quantize(lp, 1 << 16)
+    assert cdf.shape == (2, 20)
+    f = np.diff(cdf.astype(np.int64), axis=-1)
+    assert (f[:, :18] == f_alpha).all()
+    assert (f[:, 18] == f_esc).all()
+    assert (cdf[:, 0] == 0).all() and (cdf[:, -1] == 65536).all()
+
+
 def test_quantize_invariants():
     rng = np.random.default_rng(0)
     for scale in (0.1, 1.0, 5.0, 30.0):
@@ -137,6 +227,13 @@ def test_quantize_all_mass_on_one_symbol():
     lp[0, 5] = 0.0
     f = np.diff(coder.quantize(lp).astype(np.int64))[0]
     assert f[5] == 65536 - 17 and (np.delete(f, [5, 17]) == 1).all() and f[17] == 1
+
+
+def test_quantize_all_mass_on_one_symbol_18_symbols():
+    lp = np.full((1, 18), -200.0, np.float32)
+    lp[0, 17] = 0.0
+    f = np.diff(coder.quantize(lp).astype(np.int64))[0]
+    assert f[17] == 65536 - 18 and (f[:17] == 1).all() and f[18] == 1
 
 
 # -------------------------------------------------------- arithmetic coder --

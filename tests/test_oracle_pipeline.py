@@ -1,4 +1,5 @@
 """End-to-end pins of the oracle codec and of the seeded input generators."""
+import dataclasses
 import math
 
 import numpy as np
@@ -7,7 +8,7 @@ import pytest
 from oracle import coder, pipeline
 from oracle.forward import Model
 from synth import get_workload
-from synth.configs import hex_serial
+from synth.configs import SEPARATORS, hex_serial
 from synth.gen import gen_values, gen_weights, workload_values
 
 
@@ -80,6 +81,27 @@ def test_lossy_workload_roundtrip_small():
     model = Model(w.model, gen_weights(w.model, 1))
     buf = pipeline.compress(vals, ser, model, incremental=True)
     assert pipeline.decompress(buf, ser, model, np.uint8).tobytes() == vals.tobytes()
+
+
+@pytest.mark.parametrize("variant", ["H_c", "H_semi", "H_c+s"])
+def test_separator_variant_roundtrip(tiny, variant):
+    """Sec. 5.2 serialisations: H_c+s codes two separator tokens per group with
+    an 18-symbol alphabet (19 bins with the escape) and stores the second id in
+    the container."""
+    w, model, vals = tiny
+    sep, sep2 = SEPARATORS[variant]
+    ser = dataclasses.replace(w.serial, sep_id=sep, sep2_id=sep2)
+    v = vals[:60]
+    buf = pipeline.compress(v, ser, model, model_tag=3, incremental=True)
+    meta, bits, _ = pipeline.unpack_container(buf)
+    assert meta["sep_id"] == sep and meta["sep2_id"] == sep2
+    nsep = 2 if sep2 >= 0 else 1
+    assert buf[27] == 17 + nsep                            # coder bins incl. escape
+    assert len(bits) == -(-(60 * (8 + nsep)) // ser.window)
+    assert pipeline.decompress(buf, ser, model, np.float32).tobytes() == v.tobytes()
+    # full-window tables give the same stream up to float64 rounding
+    buf2 = pipeline.compress(v, ser, model, model_tag=3)
+    assert abs(len(buf2) - len(buf)) <= max(2, 0.0005 * len(buf))
 
 
 # ------------------------------------------------------- input generators --
