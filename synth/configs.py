@@ -13,7 +13,7 @@ fixed one-id-per-character map (lowercase ASCII codes for the digits, 32 for
 the space separator of the H_s variant).
 """
 from dataclasses import dataclass, field, replace
-from typing import Tuple
+from typing import List, Tuple
 
 HEX_CHARS = "0123456789abcdef"
 
@@ -78,6 +78,7 @@ class Workload:
     batch: int                    # windows per lmgc_probs call
     value_seed: int = 0
     weight_seed: int = 1
+    lossy: str = ""               # lossy steps applied before LM-GC; see parse_lossy
 
     def with_(self, **kw) -> "Workload":
         return replace(self, **kw)
@@ -120,9 +121,54 @@ LOSSY7B = Workload(
     name="lossy7b",
     model=LLAMA7B.model,
     serial=hex_serial(window=4096, bos_id=1, bytes_per_value=1),
-    n_values=8 * M, dist="topk_q8:1e-3:0.1", batch=8)
+    n_values=8 * M, dist="normal:1e-3", batch=8, lossy="sparsify:10+quantize:8")
 
 WORKLOADS = {w.name: w for w in (TINY, GPT2, TINYLLAMA, LLAMA7B, LOSSY7B)}
+
+
+# ----------------------------------------------------------- lossy steps --
+# The lossy schemes LM-GC is composed with (Section 5.4), as a '+'-joined
+# list applied left to right:
+#   sparsify:<percent>   keep that percentage of the values (float32 stream)
+#   quantize:<bits>      linear quantisation to <bits>-bit indices (Eq. 4);
+#                        1..8 bits give a uint8 stream, 9..16 a uint16 stream
+#   sign                 one sign bit per value, eight to a byte (SignSGD)
+LOSSY_VARIANTS = {
+    "q16": "quantize:16", "q8": "quantize:8", "sign": "sign",
+    "s50": "sparsify:50", "s25": "sparsify:25", "s10": "sparsify:10",
+    "s10q8": "sparsify:10+quantize:8",
+}
+
+
+def parse_lossy(spec: str) -> List[Tuple[str, int]]:
+    """'sparsify:10+quantize:8' -> [('sparsify', 10), ('quantize', 8)]."""
+    steps: List[Tuple[str, int]] = []
+    for part in filter(None, spec.split("+")):
+        name, _, arg = part.partition(":")
+        if name == "sparsify" and arg and 0 <= int(arg) <= 100:
+            steps.append((name, int(arg)))
+        elif name == "quantize" and arg and 1 <= int(arg) <= 16:
+            steps.append((name, int(arg)))
+        elif name == "sign" and not arg:
+            steps.append((name, 0))
+        else:
+            raise ValueError(f"bad lossy step {part!r}")
+    kinds = [k for k, _ in steps]
+    if ("sign" in kinds or "quantize" in kinds) and kinds[-1] not in ("sign", "quantize"):
+        raise ValueError("quantize/sign must be the last lossy step")
+    if kinds.count("sign") + kinds.count("quantize") > 1:
+        raise ValueError("at most one of quantize/sign")
+    return steps
+
+
+def lossy_bytes_per_value(spec: str) -> int:
+    """Bytes per element of the stream a lossy spec produces."""
+    steps = parse_lossy(spec)
+    if not steps or steps[-1][0] == "sparsify":
+        return 4
+    if steps[-1][0] == "sign":
+        return 1
+    return 1 if steps[-1][1] <= 8 else 2
 
 
 def get_workload(name: str) -> Workload:

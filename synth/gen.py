@@ -37,31 +37,6 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
 
 
 # ------------------------------------------------------------ value vectors --
-def _topk_zero_rest(v: np.ndarray, frac: float) -> np.ndarray:
-    """Keep the floor(frac*N) largest-magnitude entries (ties: lower index
-    first), set the rest to +0.0."""
-    n = v.size
-    k = int(np.floor(frac * n))
-    order = np.lexsort((np.arange(n), -np.abs(v.astype(np.float64))))
-    out = np.zeros_like(v)
-    keep = order[:k]
-    out[keep] = v[keep]
-    return out
-
-
-def _linear_quantize_u8(v: np.ndarray) -> np.ndarray:
-    """Linear n=8-bit quantisation of a vector to its indices (Sec. 5.4, Eq. 4):
-    (v - min) / (max - min) * (2^n - 1), rounded half-to-even, in float32."""
-    v = v.astype(np.float32)
-    mn = np.float32(v.min())
-    mx = np.float32(v.max())
-    if mx == mn:
-        return np.zeros(v.size, np.uint8)
-    t = (v - mn) / np.float32(mx - mn)
-    t = t * np.float32(255.0)
-    return np.rint(t).astype(np.uint8)
-
-
 def gen_values(dist: str, n: int, seed: int = 0) -> np.ndarray:
     """Synthetic gradient vector.
 
@@ -69,10 +44,9 @@ def gen_values(dist: str, n: int, seed: int = 0) -> np.ndarray:
       normal:<sigma>                 float32 N(0, sigma^2)
       laplace:<b>                    float32 Laplace(0, b)
       mixture:<s0>:<p>:<s1>          N(0,s0^2), replaced with prob p by N(0,s1^2)
-      topk_q8:<sigma>:<keep>         N(0,sigma^2) -> keep top fraction by
-                                     magnitude (rest +0.0) -> uint8 indices of
-                                     linear 8-bit quantisation
     Samples are drawn in float64 from default_rng(seed) and cast to float32.
+    Lossy workloads apply their sparsification/quantisation steps to this
+    vector (Workload.lossy); those steps are not part of this module.
     """
     rng = np.random.default_rng(seed)
     kind, *args = dist.split(":")
@@ -86,9 +60,6 @@ def gen_values(dist: str, n: int, seed: int = 0) -> np.ndarray:
         mask = rng.random(n) < a[1]
         outl = rng.normal(0.0, a[2], n)
         return np.where(mask, outl, base).astype(np.float32)
-    if kind == "topk_q8":
-        v = rng.normal(0.0, a[0], n).astype(np.float32)
-        return _linear_quantize_u8(_topk_zero_rest(v, a[1]))
     raise ValueError(f"unknown distribution {dist!r}")
 
 

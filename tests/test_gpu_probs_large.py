@@ -17,6 +17,7 @@ import pytest
 
 from gpu_util import build_model, log
 from oracle import coder as ocoder
+from oracle import lossy as olossy
 from oracle import pipeline as opipe
 from oracle.forward import Model as OModel
 from paper_2409_17836_amd import binding as B
@@ -107,7 +108,7 @@ def test_7b_lossy_roundtrip_short(llama7b):
     import torch
     w, model, om, _ = llama7b
     spec = hex_serial(window=64, bos_id=1, bytes_per_value=1)
-    vals = gen_values("topk_q8:1e-3:0.1", 100, 3)             # 300 tokens -> 5 windows
+    vals = olossy.prepare(gen_values("normal:1e-3", 100, 3), "sparsify:10+quantize:8")  # 5 windows
     sp = B.serial_params(spec)
     dv = torch.from_numpy(vals).cuda()
     buf = B.compress(model, dv, sp, batch=4, model_tag=77)

@@ -6,6 +6,7 @@ import pytest
 
 from gpu_util import log
 from oracle import coder as ocoder
+from oracle import lossy as olossy
 from paper_2409_17836_amd import binding as B
 from synth import get_workload
 from synth.configs import SEPARATORS, hex_serial
@@ -43,7 +44,7 @@ def test_serialize_workloads(name):
 def test_serialize_lossy_workload():
     w = get_workload("lossy7b")
     vals = gen_values(w.dist, 1 << 20, w.value_seed)       # a 1M-value slice of the 8M vector
-    _check(vals, w.serial)
+    _check(olossy.prepare(vals, w.lossy), w.serial)
 
 
 @pytest.mark.parametrize("bpg", [0, 1, 2, 3, 4, 8])

@@ -5,10 +5,10 @@ import math
 import numpy as np
 import pytest
 
-from oracle import coder, pipeline
+from oracle import coder, lossy, pipeline
 from oracle.forward import Model
 from synth import get_workload
-from synth.configs import SEPARATORS, hex_serial
+from synth.configs import LOSSY_VARIANTS, SEPARATORS, hex_serial, lossy_bytes_per_value
 from synth.gen import gen_values, gen_weights, workload_values
 
 
@@ -73,14 +73,19 @@ def test_corrupt_container_is_rejected(tiny):
         pass
 
 
-def test_lossy_workload_roundtrip_small():
-    """8-bit indices, 2 digits + separator per value (uint8 stream)."""
+@pytest.mark.parametrize("variant", sorted(LOSSY_VARIANTS))
+def test_lossy_variant_roundtrip_small(variant):
+    """Sec. 5.4 streams: 8-bit indices (2 digits + separator), 16-bit indices
+    (4 digits + separator), packed sign bytes, sparsified float32."""
     w = get_workload("tiny")
-    ser = hex_serial(window=64, bos_id=1, bytes_per_value=1)
-    vals = gen_values("topk_q8:1e-3:0.1", 500, seed=3)
+    spec = LOSSY_VARIANTS[variant]
+    bpv = lossy_bytes_per_value(spec)
+    ser = hex_serial(window=64, bos_id=1, bytes_per_value=bpv)
+    vals = lossy.prepare(gen_values("normal:1e-3", 160, seed=3), spec)
     model = Model(w.model, gen_weights(w.model, 1))
     buf = pipeline.compress(vals, ser, model, incremental=True)
-    assert pipeline.decompress(buf, ser, model, np.uint8).tobytes() == vals.tobytes()
+    back = pipeline.decompress(buf, ser, model, vals.dtype)
+    assert back.dtype == vals.dtype and back.tobytes() == vals.tobytes()
 
 
 @pytest.mark.parametrize("variant", ["H_c", "H_semi", "H_c+s"])
@@ -115,19 +120,3 @@ def test_value_distributions():
     assert abs(frac_big - 0.01 * math.erfc(0.1 / math.sqrt(2))) < 2e-3
     np.testing.assert_array_equal(gen_values("laplace:1e-3", 100, 5),
                                   gen_values("laplace:1e-3", 100, 5))
-
-
-def test_sparsify_and_quantize_generator():
-    n = 100000
-    q = gen_values("topk_q8:1e-3:0.1", n, 0)
-    assert q.dtype == np.uint8
-    assert q.min() == 0 and q.max() == 255                   # Eq. 4: min -> 0, max -> 2^n - 1
-    zero_code = np.bincount(q, minlength=256).argmax()       # the 90% zeros share one code
-    assert np.sum(q == zero_code) >= 0.9 * n
-    v = np.random.default_rng(0).normal(0, 1e-3, n).astype(np.float32)
-    k = n // 10
-    thr = np.sort(np.abs(v))[-k]
-    kept = np.abs(v) >= thr
-    # codes of kept values are monotone in the value
-    order = np.argsort(v[kept], kind="stable")
-    assert (np.diff(q[kept][order].astype(int)) >= 0).all()
