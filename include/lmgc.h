@@ -116,6 +116,63 @@ int lmgc_serialize(const void* d_values, int64_t n_values, const lmgc_serial_par
 int lmgc_deserialize(const uint8_t* sym, int64_t n_tokens, int64_t n_values,
                      const lmgc_serial_params* p, void* values_out);
 
+/* ------------------------------------------------------------ lossy steps */
+/*
+ * Lossy gradient compression that LM-GC is composed with (Sec. 5.4,
+ * "Compatibility"): sparsification keeping a given share of the values,
+ * linear quantisation to n-bit indices (Eq. 4), and one sign bit per value
+ * (the 1-bit case, SignSGD).  Their outputs are value streams for
+ * lmgc_serialize / lmgc_compress: float32 (bytes_per_value 4), uint8 indices
+ * (1) and uint16 indices (2), packed sign bytes (1).
+ *
+ * Device pointers must be 16-byte aligned; n_values <= 2^31 - 1.
+ */
+
+/* Device workspace bytes of lmgc_sparsify_topk and lmgc_quantize_linear
+ * (a few tens of KiB, independent of n_values), or < 0 if n_values is bad. */
+int64_t lmgc_lossy_workspace(int64_t n_values);
+
+/*
+ * Sparsification (Sec. 5.4): keep the k values of largest magnitude, write
+ * +0.0 in place of every other value; the stream keeps its length.
+ * Magnitude is the IEEE bit pattern with the sign bit cleared, read as an
+ * unsigned integer (the order of |v| for numbers, +0.0 and -0.0 equal, NaN
+ * above infinity).  Ties are kept in index order (lower index first).
+ *   d_values: float32 [n_values];  d_out: float32 [n_values], may equal
+ *   d_values (in place) but must not overlap it otherwise.
+ *   k: number kept, 0 <= k; k >= n_values keeps everything.  The paper's
+ *   "keep p percent" is k = floor(n_values * p / 100).
+ * GPU, async on stream (a chain of small launches: four histogram passes,
+ * a tie count and one ordered write).  Errors: EINVAL, ESIZE (workspace).
+ */
+int lmgc_sparsify_topk(const float* d_values, int64_t n_values, int64_t k, float* d_out,
+                       void* d_workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Linear quantisation (Sec. 5.4, Eq. 4) of d_values to bits-bit indices:
+ * idx = round-half-even(((v - min) / (max - min)) * (2^bits - 1)), each
+ * operation in float32 with one rounding and no fused multiply-add; min and
+ * max over the whole vector.  A constant vector gives all zeros.
+ *   bits: 1..16.  d_indices: uint8 [n_values] for bits <= 8, uint16
+ *   [n_values] for bits > 8.
+ *   min_max: nullable host float[2]; receives (min, max), the values a
+ *   receiver needs to map indices back.
+ * Synchronises the stream once (min and max are read back to validate them)
+ * and then enqueues the quantisation.  Errors: EINVAL (bad arguments, or the
+ * vector holds a NaN or an infinity), ESIZE (workspace), EDEVICE.
+ */
+int lmgc_quantize_linear(const float* d_values, int64_t n_values, int32_t bits, void* d_indices,
+                         float* min_max, void* d_workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * One sign bit per value (Sec. 5.4, the 1-bit case read as SignSGD): the
+ * IEEE sign bit (1 for negative numbers and -0.0), eight values per byte,
+ * the first value in the most significant bit, the last byte padded with
+ * zero bits.  d_out: uint8 [ceil(n_values / 8)].
+ * GPU, async on stream.  Errors: EINVAL.
+ */
+int lmgc_sign_pack(const float* d_values, int64_t n_values, uint8_t* d_out, void* stream);
+
 /* ------------------------------------------------------------------ model */
 enum { LMGC_ARCH_LLAMA = 0, LMGC_ARCH_GPT2 = 1 };
 enum { LMGC_DTYPE_F32 = 0, LMGC_DTYPE_BF16 = 1 };

@@ -10,7 +10,7 @@ OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblmgc.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["serialize.hip", "elementwise.hip", "gemm_bf16.hip", "gemm_f32.hip",
+SOURCES = ["serialize.hip", "lossy.hip", "elementwise.hip", "gemm_bf16.hip", "gemm_f32.hip",
            "attention.hip", "coder.cpp", "api.cpp"]
 
 FLAGS = [

@@ -74,6 +74,10 @@ def lib():
         "lmgc_num_windows": (i64, [i64, P(SerialParams)]),
         "lmgc_serialize": (ctypes.c_int, [vp, i64, P(SerialParams), i64, i64, vp, vp, vp]),
         "lmgc_deserialize": (ctypes.c_int, [vp, i64, i64, P(SerialParams), vp]),
+        "lmgc_lossy_workspace": (i64, [i64]),
+        "lmgc_sparsify_topk": (ctypes.c_int, [vp, i64, i64, vp, vp, sz, vp]),
+        "lmgc_quantize_linear": (ctypes.c_int, [vp, i64, i32, vp, P(ctypes.c_float), vp, sz, vp]),
+        "lmgc_sign_pack": (ctypes.c_int, [vp, i64, vp, vp]),
         "lmgc_model_num_tensors": (i32, [P(ModelConfig)]),
         "lmgc_model_tensor_info": (ctypes.c_int, [P(ModelConfig), i32, ctypes.c_char_p, sz,
                                                   P(i32), P(i64)]),
@@ -200,6 +204,77 @@ def deserialize(sym: np.ndarray, n_values: int, sp: SerialParams, dtype) -> np.n
     _check(lib().lmgc_deserialize(s.ctypes.data, s.size, n_values, ctypes.byref(sp),
                                   out.ctypes.data))
     return out.view(dtype)
+
+
+# ------------------------------------------------------------ lossy steps --
+def lossy_workspace(n_values: int) -> int:
+    n = int(lib().lmgc_lossy_workspace(n_values))
+    if n < 0:
+        _check(n)
+    return n
+
+
+def sparsify_topk(values, k: int, out=None, ws=None, stream=None):
+    """Keep the k largest-magnitude values of a CUDA float32 vector (Sec. 5.4);
+    out may be values itself."""
+    import torch
+    assert values.dtype == torch.float32 and values.is_contiguous()
+    n = values.numel()
+    if out is None:
+        out = torch.empty_like(values)
+    if ws is None:
+        ws = workspace(lossy_workspace(n), values.device)
+    _check(lib().lmgc_sparsify_topk(_ptr(values), n, int(k), _ptr(out), _ptr(ws), ws.numel(),
+                                    _stream(stream)))
+    return out
+
+
+def quantize_linear(values, bits: int, out=None, ws=None, stream=None):
+    """Eq. 4 indices of a CUDA float32 vector -> (indices, min, max).  Indices
+    are uint8 for bits <= 8, else int16 storage holding uint16 values."""
+    import torch
+    assert values.dtype == torch.float32 and values.is_contiguous()
+    n = values.numel()
+    if out is None:
+        out = torch.empty(n, dtype=torch.uint8 if bits <= 8 else torch.int16, device=values.device)
+    if ws is None:
+        ws = workspace(lossy_workspace(n), values.device)
+    mm = (ctypes.c_float * 2)()
+    _check(lib().lmgc_quantize_linear(_ptr(values), n, int(bits), _ptr(out), mm, _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+    return out, float(mm[0]), float(mm[1])
+
+
+def sign_pack(values, out=None, stream=None):
+    """SignSGD bits of a CUDA float32 vector, eight per byte, first value in bit 7."""
+    import torch
+    assert values.dtype == torch.float32 and values.is_contiguous()
+    n = values.numel()
+    if out is None:
+        out = torch.empty((n + 7) // 8, dtype=torch.uint8, device=values.device)
+    _check(lib().lmgc_sign_pack(_ptr(values), n, _ptr(out), _stream(stream)))
+    return out
+
+
+def lossy_prepare(values, steps, stream=None):
+    """Apply lossy steps [(kind, arg)] left to right on the GPU: ("sparsify",
+    percent), ("quantize", bits), ("sign", 0).  Returns the value stream."""
+    x = values
+    ws = None
+    for kind, arg in steps:
+        if kind == "sparsify":
+            if ws is None:
+                ws = workspace(lossy_workspace(x.numel()), x.device)
+            x = sparsify_topk(x, x.numel() * int(arg) // 100, ws=ws, stream=stream)
+        elif kind == "quantize":
+            if ws is None:
+                ws = workspace(lossy_workspace(x.numel()), x.device)
+            x = quantize_linear(x, int(arg), ws=ws, stream=stream)[0]
+        elif kind == "sign":
+            x = sign_pack(x, stream=stream)
+        else:
+            raise ValueError(f"unknown lossy step {kind!r}")
+    return x
 
 
 # ------------------------------------------------------------------ model --

@@ -905,6 +905,81 @@ int lmgc_deserialize(const uint8_t* sym, int64_t n_tokens, int64_t n_values, con
   return deserialize_bins(sym, n_tokens, n_values, *p, (uint8_t*)values_out);
 }
 
+static int check_lossy_vec(const float* d_values, int64_t n_values, const void* d_out) {
+  if (n_values < 0 || n_values > INT32_MAX) return set_error(LMGC_EINVAL, "n_values must be in [0, 2^31 - 1]");
+  if (n_values > 0 && (!d_values || !d_out)) return set_error(LMGC_EINVAL, "bad buffers");
+  if (((uintptr_t)d_values & 15) || ((uintptr_t)d_out & 15))
+    return set_error(LMGC_EINVAL, "device buffers must be 16-byte aligned");
+  return LMGC_OK;
+}
+
+static int check_lossy_ws(const void* ws, size_t bytes) {
+  if (!ws || bytes < lossy_workspace_bytes())
+    return set_error(LMGC_ESIZE, "lossy workspace needs %zu bytes", lossy_workspace_bytes());
+  if ((uintptr_t)ws & 15) return set_error(LMGC_EINVAL, "workspace must be 16-byte aligned");
+  return LMGC_OK;
+}
+
+int64_t lmgc_lossy_workspace(int64_t n_values) {
+  clear_error();
+  if (n_values < 0 || n_values > INT32_MAX) return set_error(LMGC_EINVAL, "n_values must be in [0, 2^31 - 1]");
+  return (int64_t)lossy_workspace_bytes();
+}
+
+int lmgc_sparsify_topk(const float* d_values, int64_t n_values, int64_t k, float* d_out, void* d_workspace,
+                       size_t workspace_bytes, void* stream) {
+  clear_error();
+  int rc = check_lossy_vec(d_values, n_values, d_out);
+  if (rc) return rc;
+  if (k < 0) return set_error(LMGC_EINVAL, "k must be >= 0");
+  if (d_out != d_values && n_values > 0 &&
+      (const char*)d_out < (const char*)(d_values + n_values) && (const char*)d_values < (const char*)(d_out + n_values))
+    return set_error(LMGC_EINVAL, "d_out overlaps d_values without being equal to it");
+  if (n_values == 0) return LMGC_OK;
+  if (k > 0 && (rc = check_lossy_ws(d_workspace, workspace_bytes))) return rc;
+  hipError_t e = launch_sparsify_topk(d_values, n_values, k, d_out, d_workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return set_error(LMGC_EDEVICE, "sparsify launch: %s", hipGetErrorString(e));
+  return LMGC_OK;
+}
+
+int lmgc_quantize_linear(const float* d_values, int64_t n_values, int32_t bits, void* d_indices, float* min_max,
+                         void* d_workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  int rc = check_lossy_vec(d_values, n_values, d_indices);
+  if (rc) return rc;
+  if (bits < 1 || bits > 16) return set_error(LMGC_EINVAL, "bits must be in [1, 16]");
+  if (n_values == 0) {
+    if (min_max) min_max[0] = min_max[1] = 0.0f;
+    return LMGC_OK;
+  }
+  if ((rc = check_lossy_ws(d_workspace, workspace_bytes))) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  LossyMinMax* slot = lossy_minmax_slot(d_workspace);
+  hipError_t e = launch_minmax(d_values, n_values, d_workspace, slot, s);
+  LossyMinMax mm{};
+  if (e == hipSuccess) e = hipMemcpyAsync(&mm, slot, sizeof(mm), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return set_error(LMGC_EDEVICE, "quantize min/max: %s", hipGetErrorString(e));
+  if (mm.nonfinite) return set_error(LMGC_EINVAL, "values hold %u NaN or infinite entries", mm.nonfinite);
+  e = launch_quantize_linear(d_values, n_values, bits, mm.mn, mm.mx, d_indices, s);
+  if (e != hipSuccess) return set_error(LMGC_EDEVICE, "quantize launch: %s", hipGetErrorString(e));
+  if (min_max) {
+    min_max[0] = mm.mn;
+    min_max[1] = mm.mx;
+  }
+  return LMGC_OK;
+}
+
+int lmgc_sign_pack(const float* d_values, int64_t n_values, uint8_t* d_out, void* stream) {
+  clear_error();
+  if (n_values < 0 || n_values > INT32_MAX) return set_error(LMGC_EINVAL, "n_values must be in [0, 2^31 - 1]");
+  if (n_values > 0 && (!d_values || !d_out)) return set_error(LMGC_EINVAL, "bad buffers");
+  if ((uintptr_t)d_values & 15) return set_error(LMGC_EINVAL, "d_values must be 16-byte aligned");
+  hipError_t e = launch_sign_pack(d_values, n_values, d_out, (hipStream_t)stream);
+  if (e != hipSuccess) return set_error(LMGC_EDEVICE, "sign pack launch: %s", hipGetErrorString(e));
+  return LMGC_OK;
+}
+
 int32_t lmgc_model_num_tensors(const lmgc_model_config* cfg) {
   clear_error();
   if (check_config(cfg)) return -1;

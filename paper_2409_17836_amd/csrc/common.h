@@ -101,6 +101,22 @@ hipError_t launch_attention_f32(const float* q, const float* k, const float* v, 
 hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
                           int n_alpha, uint32_t total, uint32_t* cdf, float* logp, hipStream_t s);
 
+// Lossy steps (lossy.hip).  The workspace holds the top-k select state, the
+// per-chunk tie counts and the min/max partials; its size does not depend on n.
+struct LossyMinMax {
+  float mn, mx;
+  uint32_t nonfinite;  // values that are NaN or infinite
+  uint32_t pad;
+};
+size_t lossy_workspace_bytes();
+hipError_t launch_sparsify_topk(const float* v, int64_t n, int64_t k, float* out, void* ws, hipStream_t s);
+// Writes the vector's LossyMinMax to res (device memory, e.g. lossy_minmax_slot(ws)).
+hipError_t launch_minmax(const float* v, int64_t n, void* ws, LossyMinMax* res, hipStream_t s);
+LossyMinMax* lossy_minmax_slot(void* ws);
+hipError_t launch_quantize_linear(const float* v, int64_t n, int bits, float mn, float mx, void* idx,
+                                  hipStream_t s);
+hipError_t launch_sign_pack(const float* v, int64_t n, uint8_t* out, hipStream_t s);
+
 // dst[r, :] = srcs.p[idx[r] >> 28][(idx[r] & 0x0fffffff), :] for r < rows;
 // idx[r] == -1 gives a zero row.  Rows are cols * elem_bytes bytes (multiple of 4).
 struct GatherSrcs {

@@ -6,11 +6,13 @@ import numpy as np
 import pytest
 
 from gpu_util import build_model, log
+from oracle import lossy as olossy
 from oracle import pipeline as opipe
 from oracle.forward import Model as OModel
 from paper_2409_17836_amd import binding as B
 from synth import get_workload
-from synth.configs import SEPARATORS, hex_serial
+from synth import parse_lossy
+from synth.configs import LOSSY_VARIANTS, SEPARATORS, hex_serial, lossy_bytes_per_value
 from synth.gen import gen_values, workload_values
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(600)]
@@ -19,7 +21,7 @@ pytestmark = [pytest.mark.gpu, pytest.mark.timeout(600)]
 def _roundtrip(model, om, vals, spec, batch, tag=5, dtype=np.float32):
     import torch
     sp = B.serial_params(spec)
-    dv = torch.from_numpy(vals).cuda()
+    dv = torch.from_numpy(vals.view(np.int16) if vals.dtype == np.uint16 else vals).cuda()
     buf = B.compress(model, dv, sp, batch=batch, model_tag=tag)
     ref = opipe.compress(vals, spec, om, model_tag=tag)
     log(f"compressed {vals.nbytes} B -> {len(buf)} B (oracle {len(ref)} B)")
@@ -60,6 +62,27 @@ def test_tiny_separator_variants():
         spec = hex_serial(window=256, bos_id=1, sep_id=sep, sep2_id=sep2)
         buf = _roundtrip(model, om, vals, spec, batch=4)
         assert buf[27] == (19 if sep2 >= 0 else 18)
+    model.close()
+
+
+@pytest.mark.parametrize("variant", ["q16", "sign", "s50", "s25"])
+def test_tiny_lossy_variants(variant):
+    """Sec. 5.4 streams prepared on the GPU: 16-bit indices (4 digits +
+    separator), packed sign bytes, sparsified float32 at 50 and 25 percent."""
+    import torch
+    w = get_workload("tiny")
+    model, host = build_model(w.model, w.weight_seed)
+    om = OModel(w.model, host)
+    lossy = LOSSY_VARIANTS[variant]
+    raw = gen_values("laplace:1e-3", 400, 12)
+    dv = B.lossy_prepare(torch.from_numpy(raw).cuda(), parse_lossy(lossy))
+    vals = olossy.prepare(raw, lossy)
+    got = dv.cpu().numpy()
+    assert got.tobytes() == vals.tobytes()
+    bpv = lossy_bytes_per_value(lossy)
+    spec = hex_serial(window=256, bos_id=1, bytes_per_value=bpv)
+    log(f"lossy variant {variant}: {vals.size} values of {bpv} bytes")
+    _roundtrip(model, om, vals, spec, batch=8, dtype=vals.dtype)
     model.close()
 
 

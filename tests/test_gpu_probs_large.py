@@ -21,7 +21,7 @@ from oracle import lossy as olossy
 from oracle import pipeline as opipe
 from oracle.forward import Model as OModel
 from paper_2409_17836_amd import binding as B
-from synth import get_workload
+from synth import get_workload, parse_lossy
 from synth.configs import hex_serial
 from synth.gen import gen_values, workload_values
 
@@ -108,9 +108,11 @@ def test_7b_lossy_roundtrip_short(llama7b):
     import torch
     w, model, om, _ = llama7b
     spec = hex_serial(window=64, bos_id=1, bytes_per_value=1)
-    vals = olossy.prepare(gen_values("normal:1e-3", 100, 3), "sparsify:10+quantize:8")  # 5 windows
+    raw = gen_values("normal:1e-3", 100, 3)                    # 300 tokens -> 5 windows
+    dv = B.lossy_prepare(torch.from_numpy(raw).cuda(), parse_lossy("sparsify:10+quantize:8"))
+    vals = olossy.prepare(raw, "sparsify:10+quantize:8")
+    assert dv.cpu().numpy().tobytes() == vals.tobytes()
     sp = B.serial_params(spec)
-    dv = torch.from_numpy(vals).cuda()
     buf = B.compress(model, dv, sp, batch=4, model_tag=77)
     back = B.decode(model, buf, batch=4, model_tag=77, dtype=np.uint8)
     assert back.tobytes() == vals.tobytes()

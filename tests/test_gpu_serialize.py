@@ -8,7 +8,7 @@ from gpu_util import log
 from oracle import coder as ocoder
 from oracle import lossy as olossy
 from paper_2409_17836_amd import binding as B
-from synth import get_workload
+from synth import get_workload, parse_lossy
 from synth.configs import SEPARATORS, hex_serial
 from synth.gen import gen_values, workload_values
 
@@ -44,7 +44,12 @@ def test_serialize_workloads(name):
 def test_serialize_lossy_workload():
     w = get_workload("lossy7b")
     vals = gen_values(w.dist, 1 << 20, w.value_seed)       # a 1M-value slice of the 8M vector
-    _check(olossy.prepare(vals, w.lossy), w.serial)
+    import torch
+    prepped = B.lossy_prepare(torch.from_numpy(vals).cuda(), parse_lossy(w.lossy))
+    want = olossy.prepare(vals, w.lossy)
+    got = prepped.cpu().numpy()
+    assert got.tobytes() == want.tobytes()
+    _check(want, w.serial)
 
 
 @pytest.mark.parametrize("bpg", [0, 1, 2, 3, 4, 8])
