@@ -25,6 +25,12 @@
  *     double from the float32 log-probability; if the A frequencies sum past
  *     T-1 the largest (lowest index on ties) gives up the excess; the escape
  *     bin takes T - sum;
+ *   - renormalised tables (the LM's distribution restricted to the alphabet
+ *     and renormalised over it, so the escape bin is empty): lp_a is the
+ *     log-probability within the alphabet, f_a = 1 + floor(exp(lp_a) * (T - A)),
+ *     the largest f_a (lowest index on ties) takes T - sum, whatever its
+ *     sign, and the escape bin has width 0 (cdf[A] = cdf[A+1] = T), which
+ *     codes exactly as an A-bin table;
  *   - coder: 62-bit code values, E1/E2/E3 renormalisation with pending bits,
  *     flush = pending+1 then one bit chosen by low < quarter; bits are packed
  *     most significant first, the last byte padded with zero bits; the
@@ -152,34 +158,38 @@ int64_t orc_hex_roundtrip_range(uint64_t lo, uint64_t hi, int32_t msb_first) {
 
 /*
  * lp[na]: float32 natural-log probabilities of the na alphabet symbols (16
- * digits and the separator token(s)); escape bin na takes the rest.
+ * digits and the separator token(s)); escape bin na takes the rest, or
+ * nothing when renorm is set (lp then sums to one over the alphabet).
  * cdf[na+2]: cdf[0] = 0, cdf[k+1] = cdf[k] + f_k, cdf[na+1] = total.
  */
-void orc_quantize(const float* lp, int32_t na, uint32_t total, uint32_t* cdf) {
-  uint32_t f[ORC_NSYM_MAX];
+void orc_quantize(const float* lp, int32_t na, int32_t renorm, uint32_t total, uint32_t* cdf) {
+  int64_t f[ORC_NSYM_MAX];
   const int32_t nsym = na + 1;
-  uint64_t s = 0;
+  const uint32_t spread = renorm ? total - (uint32_t)na : total - (uint32_t)nsym;
+  const int64_t alpha_total = renorm ? (int64_t)total : (int64_t)total - 1;
+  int64_t s = 0;
   for (int a = 0; a < na; a++) {
     double p = exp((double)lp[a]);
-    double q = floor(p * (double)(total - nsym));
-    f[a] = 1u + (uint32_t)q;
+    double q = floor(p * (double)spread);
+    f[a] = 1 + (int64_t)q;
     s += f[a];
   }
-  if (s > (uint64_t)(total - 1)) {
+  if (s > alpha_total || (renorm && s < alpha_total)) {
     int big = 0;
     for (int a = 1; a < na; a++)
       if (f[a] > f[big]) big = a;
-    f[big] -= (uint32_t)(s - (total - 1));
-    s = total - 1;
+    f[big] += alpha_total - s;
+    s = alpha_total;
   }
-  f[na] = total - (uint32_t)s;
+  f[na] = (int64_t)total - s;
   cdf[0] = 0;
-  for (int k = 0; k < nsym; k++) cdf[k + 1] = cdf[k] + f[k];
+  for (int k = 0; k < nsym; k++) cdf[k + 1] = cdf[k] + (uint32_t)f[k];
 }
 
-void orc_quantize_rows(const float* lp, int64_t rows, int32_t na, uint32_t total, uint32_t* cdf) {
+void orc_quantize_rows(const float* lp, int64_t rows, int32_t na, int32_t renorm, uint32_t total,
+                       uint32_t* cdf) {
   for (int64_t r = 0; r < rows; r++)
-    orc_quantize(lp + r * na, na, total, cdf + r * (na + 2));
+    orc_quantize(lp + r * na, na, renorm, total, cdf + r * (na + 2));
 }
 
 /* ------------------------------------------------------------------------ */

@@ -49,7 +49,7 @@ def lib():
         L.orc_hex_roundtrip_range.restype = i64
         L.orc_hex_roundtrip_range.argtypes = [u64, u64, i32]
         L.orc_quantize_rows.restype = None
-        L.orc_quantize_rows.argtypes = [vp, i64, i32, u32, vp]
+        L.orc_quantize_rows.argtypes = [vp, i64, i32, i32, u32, vp]
         L.orc_ac_encode.restype = i64
         L.orc_ac_encode.argtypes = [vp, i32, vp, i64, vp, u64]
         L.orc_decoder_size.restype = ctypes.c_size_t
@@ -117,15 +117,16 @@ def hex_roundtrip_all(msb_first: int = 1, threads: int = None) -> int:
 
 
 # -------------------------------------------------------------- quantiser --
-def quantize(lp: np.ndarray, total: int = 1 << 16) -> np.ndarray:
+def quantize(lp: np.ndarray, total: int = 1 << 16, renorm: bool = False) -> np.ndarray:
     """lp [..., A] float32 log-probs of the A alphabet symbols (17, or 18 with
-    a two-token separator) -> cdf [..., A + 2] uint32."""
+    a two-token separator) -> cdf [..., A + 2] uint32.  renorm: lp is
+    normalised over the alphabet and the escape bin is empty."""
     a = np.ascontiguousarray(lp, dtype=np.float32)
     na = a.shape[-1]
     assert na in (17, 18)
     rows = a.size // na
     out = np.empty(a.shape[:-1] + (na + 2,), np.uint32)
-    lib().orc_quantize_rows(_p(a), rows, na, total, _p(out))
+    lib().orc_quantize_rows(_p(a), rows, na, 1 if renorm else 0, total, _p(out))
     return out
 
 

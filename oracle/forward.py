@@ -210,16 +210,21 @@ class Model:
         """x: [..., n] -> logits [..., n, V]."""
         return self.final_hidden(x) @ self.head_matrix().T
 
-    def alphabet_logprobs(self, x: np.ndarray, ids) -> np.ndarray:
+    def alphabet_logprobs(self, x: np.ndarray, ids, renorm: bool = False) -> np.ndarray:
         """x: [..., n] -> [..., n, len(ids)] natural-log probabilities of the
-        given ids, normalised over the whole vocabulary (Eq. 2)."""
-        return logprobs_from_logits(self.logits(x), ids)
+        given ids, normalised over the whole vocabulary (Eq. 2), or over the
+        given ids only (renorm)."""
+        return logprobs_from_logits(self.logits(x), ids, renorm)
 
 
-def logprobs_from_logits(z: np.ndarray, ids) -> np.ndarray:
-    mx = z.max(axis=-1, keepdims=True)
-    lse = mx + np.log(np.sum(np.exp(z - mx), axis=-1, keepdims=True))
-    return z[..., np.asarray(ids)] - lse
+def logprobs_from_logits(z: np.ndarray, ids, renorm: bool = False) -> np.ndarray:
+    """log softmax of the logits at ids; over the whole vocabulary, or, with
+    renorm, over the ids alone (the distribution restricted to them)."""
+    za = z[..., np.asarray(ids)]
+    zn = za if renorm else z
+    mx = zn.max(axis=-1, keepdims=True)
+    lse = mx + np.log(np.sum(np.exp(zn - mx), axis=-1, keepdims=True))
+    return za - lse
 
 
 # ---------------------------------------------------- incremental (decode) --

@@ -29,6 +29,12 @@ def _sep2(serial) -> int:
     return int(getattr(serial, "sep2_id", -1))
 
 
+def _renorm(serial) -> bool:
+    """Tables of the LM's distribution renormalised over the alphabet (no
+    escape mass) instead of the full-vocabulary distribution."""
+    return bool(getattr(serial, "renorm", 0))
+
+
 def alphabet_ids(serial) -> List[int]:
     """Token ids of the coder bins before the escape: the 16 hex digits, the
     separator, and the second separator token if there is one (H_c+s)."""
@@ -62,7 +68,8 @@ def model_input(tok_window: np.ndarray, serial, length: int = None) -> np.ndarra
 def window_logprobs(model: Model, tok_window: np.ndarray, serial, n_pos: int = None) -> np.ndarray:
     """[n_pos, A] log-probs of the alphabet at positions 0..n_pos-1."""
     n = tok_window.size if n_pos is None else n_pos
-    return model.alphabet_logprobs(model_input(tok_window, serial, n), alphabet_ids(serial))
+    return model.alphabet_logprobs(model_input(tok_window, serial, n), alphabet_ids(serial),
+                                   _renorm(serial))
 
 
 # ---------------------------------------------------------------- container --
@@ -72,8 +79,8 @@ def pack_container(serial, n_values: int, model_tag: int, total: int,
     hdr = struct.pack("<4sHHQQBBBBIII", MAGIC, VERSION, HEADER_BYTES, model_tag,
                       n_values, serial.bytes_per_value, serial.bytes_per_group,
                       serial.msb_first, nsym, serial.window, total, len(bits))
-    hdr += struct.pack("<iii16iI", serial.bos_id, serial.pad_id, serial.sep_id,
-                       *serial.hex_ids, _sep2(serial) + 1)
+    hdr += struct.pack("<iii16iII", serial.bos_id, serial.pad_id, serial.sep_id,
+                       *serial.hex_ids, _sep2(serial) + 1, int(_renorm(serial)))
     hdr += b"\0" * (HEADER_BYTES - len(hdr))
     assert len(hdr) == HEADER_BYTES
     return hdr + struct.pack(f"<{len(bits)}I", *bits) + b"".join(payloads)
@@ -84,8 +91,10 @@ def unpack_container(buf: bytes):
         raise ValueError("not an LM-GC container")
     (magic, ver, hbytes, tag, n_values, bpv, bpg, msb, nsym, W, total,
      nwin) = struct.unpack_from("<4sHHQQBBBBIII", buf, 0)
-    ids = struct.unpack_from("<iii16iI", buf, 40)
+    ids = struct.unpack_from("<iii16iII", buf, 40)
     sep2 = ids[19] - 1
+    if ids[20] > 1:
+        raise ValueError("unsupported container")
     if ver != VERSION or hbytes != HEADER_BYTES or nsym != (19 if sep2 >= 0 else 18):
         raise ValueError("unsupported container")
     off = HEADER_BYTES
@@ -102,7 +111,8 @@ def unpack_container(buf: bytes):
         off += nb
     meta = dict(model_tag=tag, n_values=n_values, bytes_per_value=bpv,
                 bytes_per_group=bpg, msb_first=msb, window=W, total=total,
-                bos_id=ids[0], pad_id=ids[1], sep_id=ids[2], hex_ids=ids[3:19], sep2_id=sep2)
+                bos_id=ids[0], pad_id=ids[1], sep_id=ids[2], hex_ids=ids[3:19], sep2_id=sep2,
+                renorm=bool(ids[20]))
     return meta, bits, payloads
 
 
@@ -120,13 +130,13 @@ def compress(values: np.ndarray, serial, model: Model, model_tag: int = 0,
         # pad tokens and, by causality, do not change the positions before it
         nmax = max(n for _, n in wins)
         X = np.stack([model_input(tok[s:s + n], serial, nmax) for s, n in wins])
-        lp = model.alphabet_logprobs(X, alphabet_ids(serial))
+        lp = model.alphabet_logprobs(X, alphabet_ids(serial), _renorm(serial))
         lp_rows = [lp[w, :n] for w, (_, n) in enumerate(wins)]
     else:
         lp_rows = []
     bits, payloads = [], []
     for (s, n), lp in zip(wins, lp_rows):
-        cdf = coder.quantize(lp.astype(np.float32), total)
+        cdf = coder.quantize(lp.astype(np.float32), total, _renorm(serial))
         pay, nb = coder.ac_encode(cdf, sym[s:s + n])
         bits.append(nb)
         payloads.append(pay)
@@ -145,7 +155,7 @@ def _incremental_logprobs(model, tok, wins, serial):
     x = np.full(nb, serial.bos_id, np.int64)
     from .forward import logprobs_from_logits
     for j in range(nmax):
-        out[:, j] = logprobs_from_logits(lm.step(x), ids)
+        out[:, j] = logprobs_from_logits(lm.step(x), ids, _renorm(serial))
         x = toks[:, j]
     return [out[w, :n] for w, (_, n) in enumerate(wins)]
 
@@ -171,8 +181,8 @@ def decompress(buf: bytes, serial, model: Model, dtype) -> np.ndarray:
     x = np.full(nb, serial.bos_id, np.int64)
     id_of = np.array(ids, np.int64)
     for j in range(nmax):
-        lp = logprobs_from_logits(lm.step(x), ids).astype(np.float32)
-        cdf = coder.quantize(lp, total)
+        lp = logprobs_from_logits(lm.step(x), ids, meta["renorm"]).astype(np.float32)
+        cdf = coder.quantize(lp, total, meta["renorm"])
         nxt = np.full(nb, serial.pad_id, np.int64)
         for w, (s, n) in enumerate(wins):
             if j < n:

@@ -48,6 +48,7 @@ class SerialSpec:
     sep_id: int
     hex_ids: Tuple[int, ...] = field(default=tuple(ord(c) for c in HEX_CHARS))
     sep2_id: int = -1             # second separator token after each group; -1 = none
+    renorm: int = 0               # 1: tables renormalised over the alphabet (no escape mass)
 
 
 # The separators of the paper's hexadecimal serialisations (Section 5.2,

@@ -236,6 +236,61 @@ def test_quantize_all_mass_on_one_symbol_18_symbols():
     assert f[17] == 65536 - 18 and (f[:17] == 1).all() and f[18] == 1
 
 
+# Renormalised tables: the LM's distribution restricted to the alphabet and
+# renormalised, no escape mass.  f_a = 1 + floor(p_a (T - A)); the largest
+# takes T - sum; the escape bin is empty.
+@pytest.mark.parametrize("A,f0,f_rest", [
+    (17, 3856, 3855),      # 65519 / 17 = 3854.06 -> 3855; sum 65535, +1 to bin 0
+    (18, 3656, 3640),      # 65518 / 18 = 3639.89 -> 3640; sum 65520, +16 to bin 0
+])
+def test_quantize_renorm_uniform_closed_form(A, f0, f_rest):
+    lp = np.full((3, A), -math.log(A), np.float32)
+    cdf = coder.quantize(lp, 1 << 16, renorm=True)
+    f = np.diff(cdf.astype(np.int64), axis=-1)
+    assert (f[:, 0] == f0).all() and (f[:, 1:A] == f_rest).all()
+    assert (f[:, A] == 0).all()                                   # empty escape bin
+    assert (cdf[:, -2] == 65536).all() and (cdf[:, -1] == 65536).all()
+
+
+def test_quantize_renorm_all_mass_and_invariants():
+    lp = np.full((1, 17), -200.0, np.float32)
+    lp[0, 3] = 0.0
+    f = np.diff(coder.quantize(lp, renorm=True).astype(np.int64))[0]
+    assert f[3] == 65536 - 16 and (np.delete(f, [3, 17]) == 1).all() and f[17] == 0
+    rng = np.random.default_rng(9)
+    for T in (38, 1 << 16, 1 << 24):
+        for A in (17, 18):
+            z = rng.normal(0, 3.0, (500, A))
+            lp = z - np.log(np.exp(z).sum(1, keepdims=True))      # normalised over the alphabet
+            lp = lp.astype(np.float32)
+            cdf = coder.quantize(lp, T, renorm=True)
+            f = np.diff(cdf.astype(np.int64), axis=-1)
+            assert (f[:, :A] >= 1).all() and (f[:, A] == 0).all() and (cdf[:, -1] == T).all()
+            p = np.exp(lp.astype(np.float64))
+            # each bin within p A + 1 of p T; the largest also absorbs T - sum <= A
+            assert np.abs(f[:, :A] - p * T).max() <= 2 * A + 2
+
+
+def test_renorm_tables_code_as_alphabet_only_tables():
+    """An empty last bin codes exactly as the same table without it, and the
+    stream stays within the Sec. 3 bound."""
+    rng = np.random.default_rng(4)
+    n = 400
+    z = rng.normal(0, 2.0, (n, 17))
+    lp = (z - np.log(np.exp(z).sum(1, keepdims=True))).astype(np.float32)
+    cdf = coder.quantize(lp, renorm=True)
+    sym = np.array([rng.choice(17, p=np.exp(r.astype(np.float64)) / np.exp(r.astype(np.float64)).sum())
+                    for r in lp], np.uint8)
+    pay, nbits = coder.ac_encode(cdf, sym)
+    pay2, nbits2 = coder.ac_encode(np.ascontiguousarray(cdf[:, :18]), sym)   # 17 bins, no escape
+    assert (pay, nbits) == (pay2, nbits2)
+    f = cdf[np.arange(n), sym.astype(int) + 1].astype(np.int64) - cdf[np.arange(n), sym].astype(np.int64)
+    H = float(-np.sum(np.log2(f / 65536.0)))
+    assert H - 1e-6 <= nbits <= H + 2 + 1e-6
+    dec = coder.StepDecoder(pay, nbits)
+    assert [dec.decode(cdf[j]) for j in range(n)] == list(sym)
+
+
 # -------------------------------------------------------- arithmetic coder --
 def _bits_str(payload, nbits):
     return "".join(f"{b:08b}" for b in payload)[:nbits]

@@ -257,3 +257,20 @@ def test_batched_windows_equal_single_windows(shape):
     batched = model.logits(x)
     for b in range(3):
         np.testing.assert_allclose(batched[b], model.logits(x[b]), rtol=0, atol=1e-12)
+
+
+def test_renormalised_logprobs_identities():
+    """Restricting to the alphabet and renormalising: lp_renorm = lp_full -
+    log sum_alphabet exp(lp_full); the renormalised probabilities sum to one;
+    with every vocabulary id as the alphabet the two modes agree."""
+    from oracle.forward import logprobs_from_logits
+    rng = np.random.default_rng(2)
+    z = rng.normal(0, 2.0, (5, 7, 40))
+    ids = [3, 0, 39, 17, 8, 21]
+    full = logprobs_from_logits(z, ids)
+    ren = logprobs_from_logits(z, ids, renorm=True)
+    np.testing.assert_allclose(ren, full - np.log(np.exp(full).sum(-1, keepdims=True)), atol=1e-12)
+    np.testing.assert_allclose(np.exp(ren).sum(-1), 1.0, atol=1e-12)
+    every = list(range(40))
+    np.testing.assert_allclose(logprobs_from_logits(z, every, renorm=True), logprobs_from_logits(z, every),
+                               atol=1e-12)

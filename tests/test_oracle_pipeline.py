@@ -109,6 +109,23 @@ def test_separator_variant_roundtrip(tiny, variant):
     assert abs(len(buf2) - len(buf)) <= max(2, 0.0005 * len(buf))
 
 
+def test_renormalised_tables_roundtrip_and_gain(tiny):
+    """Tables renormalised over the alphabet: lossless, recorded in the
+    container, and shorter than the full-vocabulary tables (the tiny model
+    puts about 239/256 of its mass outside the alphabet)."""
+    w, model, vals = tiny
+    v = vals[:60]
+    ser = dataclasses.replace(w.serial, renorm=1)
+    buf = pipeline.compress(v, ser, model, incremental=True)
+    meta, _, _ = pipeline.unpack_container(buf)
+    assert meta["renorm"] is True
+    assert pipeline.decompress(buf, ser, model, np.float32).tobytes() == v.tobytes()
+    full = pipeline.compress(v, w.serial, model, incremental=True)
+    assert len(buf) < 0.7 * len(full)
+    buf2 = pipeline.compress(v, ser, model)
+    assert abs(len(buf2) - len(buf)) <= max(2, 0.0005 * len(buf))
+
+
 # ------------------------------------------------------- input generators --
 def test_value_distributions():
     x = gen_values("normal:1e-3", 200000, 0)
