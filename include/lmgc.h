@@ -71,6 +71,13 @@ const char* lmgc_version(void);
  * coded).  The alphabet (bins before the escape) has A = 17 or 18 symbols
  * (lmgc_alphabet_size); tables have A + 2 entries.  Alphabet ids must be
  * pairwise distinct and, like bos_id and pad_id, < the model's vocabulary.
+ *
+ * Tables (Sec. 4, the LM's distribution is the coder's model): with renorm =
+ * 0 the alphabet bins carry the LM's probabilities over the whole vocabulary
+ * and the escape bin the rest; with renorm = 1 the distribution is restricted
+ * to the alphabet and renormalised over it (log-softmax over the A alphabet
+ * logits; only those A columns of the LM head are evaluated), and the escape
+ * bin is empty (cdf[A] = cdf[A+1] = total).
  */
 typedef struct {
   int32_t bytes_per_value; /* 4 (float32) | 2 | 1 (8-bit indices) */
@@ -82,6 +89,7 @@ typedef struct {
   int32_t sep_id;
   int32_t hex_ids[16];
   int32_t sep2_id;         /* second separator token, or -1 (none) */
+  int32_t renorm;          /* 0: full-vocabulary tables + escape; 1: renormalised */
 } lmgc_serial_params;
 
 #define LMGC_NALPHA 17     /* alphabet with one separator token        */
@@ -307,7 +315,7 @@ int lmgc_decode_symbol(lmgc_decoder* st, const uint32_t* cdf_row, int32_t nsym,
  *   16 u64 n_values | 24 u8 bytes_per_value | 25 u8 bytes_per_group |
  *   26 u8 msb_first | 27 u8 nsym (A + 1) | 28 u32 W | 32 u32 total |
  *   36 u32 n_windows | 40 i32 bos | 44 i32 pad | 48 i32 sep | 52 i32 hex[16] |
- *   116 u32 sep2_id + 1 (0: none) | 120..127 zero
+ *   116 u32 sep2_id + 1 (0: none) | 120 u32 renorm | 124..127 zero
  * then u32 bits[n_windows], then the payloads, each ceil(bits/8) bytes.
  */
 #define LMGC_HEADER_BYTES 128

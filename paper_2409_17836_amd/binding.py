@@ -35,7 +35,7 @@ class SerialParams(ctypes.Structure):
                 ("msb_first", ctypes.c_int32), ("window", ctypes.c_int32),
                 ("bos_id", ctypes.c_int32), ("pad_id", ctypes.c_int32),
                 ("sep_id", ctypes.c_int32), ("hex_ids", ctypes.c_int32 * 16),
-                ("sep2_id", ctypes.c_int32)]
+                ("sep2_id", ctypes.c_int32), ("renorm", ctypes.c_int32)]
 
 
 class ModelConfig(ctypes.Structure):
@@ -146,6 +146,8 @@ def serial_params(spec) -> SerialParams:
             p.hex_ids = (ctypes.c_int32 * 16)(*ids)
         elif f == "sep2_id":
             p.sep2_id = int(getattr(spec, "sep2_id", -1))
+        elif f == "renorm":
+            p.renorm = int(getattr(spec, "renorm", 0))
         else:
             setattr(p, f, int(getattr(spec, f)))
     return p

@@ -62,6 +62,7 @@ static int check_serial(const lmgc_serial_params* p, int vocab) {
   if (p->msb_first != 0 && p->msb_first != 1) return set_error(LMGC_EINVAL, "msb_first must be 0 or 1");
   if (p->window <= 0) return set_error(LMGC_EINVAL, "window must be positive");
   if (p->sep2_id < -1) return set_error(LMGC_EINVAL, "sep2_id must be -1 (none) or a token id");
+  if (p->renorm != 0 && p->renorm != 1) return set_error(LMGC_EINVAL, "renorm must be 0 or 1");
   int32_t ids[LMGC_NALPHA_MAX];
   const int na = alphabet(*p, ids);
   for (int a = 0; a < na; a++)
@@ -382,6 +383,7 @@ struct ProbsWs {
   float* h;
   void *a, *q, *k, *v, *o, *ff;
   float* logits;
+  void* head_alpha;  // [tile, d] alphabet rows of the LM head (renormalised tables)
   size_t bytes;
 };
 
@@ -403,6 +405,7 @@ static ProbsWs carve(const lmgc_model* m, int B, int W, char* base) {
   w.o = take(M * c.n_heads * m->hd * m->act);
   w.ff = take(M * c.d_ff * m->act);
   w.logits = (float*)take(M * m->v_pad * 4);
+  w.head_alpha = take((size_t)m->tile * c.d_model * m->act);
   w.bytes = off;
   return w;
 }
@@ -417,6 +420,7 @@ struct FwdBufs {
   float* h;
   void *a, *q, *o, *ff;
   float* logits;
+  void* head_alpha;
   void* const* kc;
   void* const* vc;
 };
@@ -519,6 +523,28 @@ static int forward(const lmgc_model* m, const int32_t* tok, int B, int W, int dp
     ScopedTimer t(LMGC_K_NORM, s);
     HIP_OK(launch_norm(f.h, M, d, m->final_g, m->final_b, !llama, c.norm_eps, c.dtype, f.a, s));
   }
+  int32_t ids[LMGC_NALPHA_MAX];
+  const int na = alphabet(*p, ids);
+  if (p->renorm) {
+    // Renormalised tables need only the alphabet's logits: the LM head is
+    // cut to its A alphabet rows (one N tile), and the LSE runs over them.
+    int32_t compact[LMGC_NALPHA_MAX];
+    for (int a = 0; a < na; a++) compact[a] = a;
+    {
+      ScopedTimer t(LMGC_K_GEMM_HEAD, s);
+      HIP_OK(launch_alpha_head(m->head, ids, na, m->tile, d, m->act, f.head_alpha, s));
+      EpiArgs e = {};
+      e.kind = EPI_STORE_F32;
+      e.M = M;
+      e.N = na;
+      e.c = f.logits;
+      e.ldc = m->tile;
+      HIP_OK(gemm(f.a, f.head_alpha, m->tile, d, e));
+    }
+    ScopedTimer t(LMGC_K_LSE_CDF, s);
+    HIP_OK(launch_lse_cdf(f.logits, M, m->tile, na, compact, na, total, 1, cdf, logp, s));
+    return LMGC_OK;
+  }
   {
     ScopedTimer t(LMGC_K_GEMM_HEAD, s);
     EpiArgs e = {};
@@ -531,9 +557,7 @@ static int forward(const lmgc_model* m, const int32_t* tok, int B, int W, int dp
   }
   {
     ScopedTimer t(LMGC_K_LSE_CDF, s);
-    int32_t ids[LMGC_NALPHA_MAX];
-    const int na = alphabet(*p, ids);
-    HIP_OK(launch_lse_cdf(f.logits, M, m->v_pad, c.vocab, ids, na, total, cdf, logp, s));
+    HIP_OK(launch_lse_cdf(f.logits, M, m->v_pad, c.vocab, ids, na, total, 0, cdf, logp, s));
   }
   return LMGC_OK;
 }
@@ -554,7 +578,7 @@ static int run_probs(const lmgc_model* m, const int32_t* tok, int B, int W, cons
   if (ws_bytes < w.bytes) return set_error(LMGC_ESIZE, "workspace too small: %zu < %zu", ws_bytes, w.bytes);
 
   std::vector<void*> kc(c.n_layers, w.k), vc(c.n_layers, w.v);
-  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.logits, kc.data(), vc.data()};
+  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.logits, w.head_alpha, kc.data(), vc.data()};
   return forward(m, tok, B, W, -1, p, total, f, cdf, logp, s);
 }
 
@@ -584,6 +608,7 @@ struct StepWs {
   float* h;
   void *a, *q, *o, *ff;
   float* logits;
+  void* head_alpha;  // [tile, d] alphabet rows of the LM head (renormalised tables)
   int32_t* tok;     // [B] input token of the step (the previous position's)
   uint32_t* cdf;    // [B, A + 2] (A: alphabet size)
   float* logp;      // [B, A]
@@ -607,6 +632,7 @@ static StepWs carve_step(const lmgc_model* m, int B, int W, char* base) {
   w.o = take((size_t)B * hq * act);
   w.ff = take((size_t)B * c.d_ff * act);
   w.logits = (float*)take((size_t)B * m->v_pad * 4);
+  w.head_alpha = take((size_t)m->tile * c.d_model * act);
   w.tok = (int32_t*)take((size_t)B * 4);
   w.cdf = (uint32_t*)take((size_t)B * (LMGC_NSYM_MAX + 1) * 4);
   w.logp = (float*)take((size_t)B * LMGC_NALPHA_MAX * 4);
@@ -637,7 +663,7 @@ static int check_step(const lmgc_model* m, int B, int W, const lmgc_serial_param
 // the tokens at j - 1); tables land in w.cdf (and w.logp).
 static int run_step(const lmgc_model* m, StepWs& w, int B, int W, int j, const lmgc_serial_params* p,
                     uint32_t total, bool want_logp, hipStream_t s) {
-  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.logits, w.kc.data(), w.vc.data()};
+  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.logits, w.head_alpha, w.kc.data(), w.vc.data()};
   return forward(m, w.tok, B, W, j, p, total, f, w.cdf, want_logp ? w.logp : nullptr, s);
 }
 

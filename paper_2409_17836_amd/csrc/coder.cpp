@@ -300,6 +300,7 @@ void write_header(uint8_t* h, const ContainerHeader& c) {
   put_u32(h + 48, (uint32_t)c.p.sep_id);
   for (int i = 0; i < 16; i++) put_u32(h + 52 + 4 * i, (uint32_t)c.p.hex_ids[i]);
   put_u32(h + 116, (uint32_t)(c.p.sep2_id + 1));
+  put_u32(h + 120, (uint32_t)c.p.renorm);
 }
 
 int read_header(const uint8_t* buf, size_t bytes, ContainerHeader* c) {
@@ -320,6 +321,8 @@ int read_header(const uint8_t* buf, size_t bytes, ContainerHeader* c) {
   c->p.sep_id = (int32_t)get_u32(buf + 48);
   for (int i = 0; i < 16; i++) c->p.hex_ids[i] = (int32_t)get_u32(buf + 52 + 4 * i);
   c->p.sep2_id = (int32_t)get_u32(buf + 116) - 1;
+  c->p.renorm = (int32_t)get_u32(buf + 120);
+  if (c->p.renorm != 0 && c->p.renorm != 1) return set_error(LMGC_ECORRUPT, "container: bad table mode");
   if (buf[27] != (c->p.sep2_id >= 0 ? LMGC_NALPHA_MAX + 1 : LMGC_NALPHA + 1))
     return set_error(LMGC_ECORRUPT, "container: symbol count does not match the separators");
   if (c->n_values < 0 || c->p.window <= 0 ||

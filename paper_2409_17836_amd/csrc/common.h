@@ -98,8 +98,15 @@ hipError_t launch_attention_f32(const float* q, const float* k, const float* v, 
 
 // logits [M, ldz] (first V valid) -> cdf [M, A + 2], logp [M, A] (nullable);
 // alpha_ids is a host array of the A = n_alpha (17 or 18) alphabet token ids.
+// renorm: tables renormalised over the alphabet (the logits are then the
+// alphabet's own, V = A); otherwise full-vocabulary tables with an escape bin.
 hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
-                          int n_alpha, uint32_t total, uint32_t* cdf, float* logp, hipStream_t s);
+                          int n_alpha, uint32_t total, int renorm, uint32_t* cdf, float* logp, hipStream_t s);
+
+// dst [rows, cols]: row r < n_alpha = head row alpha_ids[r] (host array),
+// the remaining rows zero.  Rows are cols * elem_bytes bytes (multiple of 4).
+hipError_t launch_alpha_head(const void* head, const int32_t* alpha_ids, int n_alpha, int rows, int cols,
+                             int elem_bytes, void* dst, hipStream_t s);
 
 // Lossy steps (lossy.hip).  The workspace holds the top-k select state, the
 // per-chunk tie counts and the min/max partials; its size does not depend on n.

@@ -161,12 +161,17 @@ __global__ void norm_bf16x4_kernel(const float* __restrict__ h, int M, const uin
 // ------------------------------------------------------------ LSE + table
 // One wave per row: online max / sum-exp over the V logits, then the NA
 // alphabet log-probabilities and their integer table of NA + 2 entries
-// (quantised in double; escape bin NA).
+// (quantised in double; escape bin NA).  renorm: the V logits are the
+// alphabet's own (V = NA), so the log-probabilities are normalised over the
+// alphabet; the largest frequency takes total - sum and the escape bin is
+// empty.
 template <int NA>
 __global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int V,
-                               AlphaIds ids, uint32_t total,
+                               AlphaIds ids, uint32_t total, int renorm,
                                uint32_t* __restrict__ cdf, float* __restrict__ logp) {
   constexpr int NS = NA + 1;  // coder bins incl. escape
+  const uint32_t spread = renorm ? total - NA : total - NS;
+  const int64_t alpha_total = renorm ? (int64_t)total : (int64_t)total - 1;
   const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (row >= M) return;
@@ -203,26 +208,26 @@ __global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int 
   if (lane < NA) {
     lp = zr[ids.v[lane]] - lse;
     const double p = exp((double)lp);
-    f = 1u + (uint32_t)floor(p * (double)(total - NS));
+    f = 1u + (uint32_t)floor(p * (double)spread);
     if (logp) logp[row * NA + lane] = lp;
   }
   uint32_t fa[NA];
-  uint64_t S = 0;
+  int64_t S = 0;
 #pragma unroll
   for (int a = 0; a < NA; a++) {
     fa[a] = (uint32_t)__shfl((int)f, a, kWave);
     S += fa[a];
   }
-  if (S > (uint64_t)(total - 1)) {
+  if (S > alpha_total || (renorm && S < alpha_total)) {
     int big = 0;
 #pragma unroll
     for (int a = 1; a < NA; a++)
       if (fa[a] > fa[big]) big = a;
-    const uint32_t ex = (uint32_t)(S - (total - 1));
+    const int64_t adj = alpha_total - S;
 #pragma unroll
     for (int a = 0; a < NA; a++)
-      if (a == big) fa[a] -= ex;
-    S = total - 1;
+      if (a == big) fa[a] = (uint32_t)((int64_t)fa[a] + adj);
+    S = alpha_total;
   }
   if (lane <= NS) {
     uint32_t c = 0;
@@ -232,6 +237,20 @@ __global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int 
     if (lane == NS) c = total;
     cdf[row * (NS + 1) + lane] = c;
   }
+}
+
+// Rows of the LM head for the alphabet tokens: dst row r (r < na) = head row
+// ids[r]; rows na..gridDim.x-1 are zero.  One block per row.
+__global__ void alpha_head_kernel(const uint32_t* __restrict__ head, AlphaIds ids, int na, int words,
+                                  uint32_t* __restrict__ dst) {
+  const int r = blockIdx.x;
+  uint32_t* out = dst + (int64_t)r * words;
+  if (r >= na) {
+    for (int c = threadIdx.x; c < words; c += blockDim.x) out[c] = 0u;
+    return;
+  }
+  const uint32_t* src = head + (int64_t)ids.v[r] * words;
+  for (int c = threadIdx.x; c < words; c += blockDim.x) out[c] = src[c];
 }
 
 // ------------------------------------------------------------------ gather
@@ -301,16 +320,29 @@ hipError_t launch_norm(const float* h, int M, int d, const void* gain, const voi
 }
 
 hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
-                          int n_alpha, uint32_t total, uint32_t* cdf, float* logp, hipStream_t s) {
+                          int n_alpha, uint32_t total, int renorm, uint32_t* cdf, float* logp,
+                          hipStream_t s) {
   AlphaIds ids = {};
   if (n_alpha != LMGC_NALPHA && n_alpha != LMGC_NALPHA_MAX) return hipErrorInvalidValue;
   for (int a = 0; a < n_alpha; a++) ids.v[a] = alpha_ids[a];
   const dim3 grid((unsigned)((M + 3) / 4)), block(256);
   if (n_alpha == LMGC_NALPHA)
-    hipLaunchKernelGGL(lse_cdf_kernel<LMGC_NALPHA>, grid, block, 0, s, logits, M, ldz, V, ids, total, cdf, logp);
-  else
-    hipLaunchKernelGGL(lse_cdf_kernel<LMGC_NALPHA_MAX>, grid, block, 0, s, logits, M, ldz, V, ids, total, cdf,
+    hipLaunchKernelGGL(lse_cdf_kernel<LMGC_NALPHA>, grid, block, 0, s, logits, M, ldz, V, ids, total, renorm, cdf,
                        logp);
+  else
+    hipLaunchKernelGGL(lse_cdf_kernel<LMGC_NALPHA_MAX>, grid, block, 0, s, logits, M, ldz, V, ids, total, renorm,
+                       cdf, logp);
+  return hipGetLastError();
+}
+
+hipError_t launch_alpha_head(const void* head, const int32_t* alpha_ids, int n_alpha, int rows, int cols,
+                             int elem_bytes, void* dst, hipStream_t s) {
+  AlphaIds ids = {};
+  if (n_alpha < 1 || n_alpha > LMGC_NALPHA_MAX || rows < n_alpha || (cols * elem_bytes) % 4)
+    return hipErrorInvalidValue;
+  for (int a = 0; a < n_alpha; a++) ids.v[a] = alpha_ids[a];
+  hipLaunchKernelGGL(alpha_head_kernel, dim3((unsigned)rows), dim3(256), 0, s, (const uint32_t*)head, ids, n_alpha,
+                     cols * elem_bytes / 4, (uint32_t*)dst);
   return hipGetLastError();
 }
 

@@ -86,6 +86,23 @@ def test_tiny_lossy_variants(variant):
     model.close()
 
 
+def test_renormalised_tables_roundtrip():
+    """Renormalised tables (no escape mass): tiny float32 and GPT-2 bf16."""
+    import dataclasses
+    w = get_workload("tiny")
+    model, host = build_model(w.model, w.weight_seed)
+    vals = gen_values("laplace:1e-3", 300, 13)
+    spec = dataclasses.replace(w.serial, renorm=1)
+    buf = _roundtrip(model, OModel(w.model, host), vals, spec, batch=8)
+    assert int.from_bytes(buf[120:124], "little") == 1
+    model.close()
+    w = get_workload("gpt2")
+    model, host = build_model(w.model, w.weight_seed, "perturbed")
+    spec = dataclasses.replace(w.serial, renorm=1)
+    _roundtrip(model, OModel(w.model, host), workload_values(w)[:250], spec, batch=2)
+    model.close()
+
+
 def test_gpt2_short_roundtrip():
     w = get_workload("gpt2")
     model, host = build_model(w.model, w.weight_seed, "perturbed")

@@ -113,6 +113,39 @@ def test_gpt2_launch_config_logprobs(gpt2):
     assert np.array_equal(cdf.cpu().numpy().view(np.uint32), ocoder.quantize(lp))
 
 
+@pytest.mark.parametrize("which", ["tiny", "gpt2"])
+def test_renormalised_tables(which, tiny_perturbed, gpt2):
+    """Tables renormalised over the alphabet (only the A alphabet columns of
+    the LM head): log-probs vs the oracle (1e-4 float32, 2e-2 bf16), tables
+    equal to the oracle's quantiser bit for bit, escape bin empty, and the
+    decoder's stepwise tables equal to the encoder's."""
+    import dataclasses
+    import torch
+    w, model, om = tiny_perturbed if which == "tiny" else gpt2
+    ser = dataclasses.replace(w.serial, renorm=1)
+    n_val = 400 if which == "tiny" else 230               # 15 windows / 3 windows
+    vals = workload_values(w)[:n_val]
+    sp = B.serial_params(ser)
+    nw = B.num_windows(vals.size, sp)
+    tok, _ = B.serialize(torch.from_numpy(vals).cuda(), sp, 0, nw)
+    cdf, logp = B.probs(model, tok, sp)
+    torch.cuda.synchronize()
+    lp = logp.cpu().numpy()
+    otok, _ = opipe.serialize(vals, ser)
+    X = np.stack([opipe.model_input(otok[s:s + n], ser, ser.window)
+                  for s, n in opipe.windows(otok.size, ser.window)])
+    ref = om.alphabet_logprobs(X, opipe.alphabet_ids(ser), renorm=True)
+    err = np.abs(lp - ref).max()
+    log(f"{which} renormalised: max |lp - oracle| = {err:.3g}")
+    assert err <= (1e-4 if which == "tiny" else 2e-2)
+    c = cdf.cpu().numpy().view(np.uint32)
+    assert np.array_equal(c, ocoder.quantize(lp, renorm=True))
+    assert (c[..., -2] == 65536).all() and (c[..., -1] == 65536).all()
+    cdf2, logp2 = B.probs_stepwise(model, tok, sp)
+    assert np.array_equal(cdf2.cpu().numpy(), cdf.cpu().numpy())
+    assert np.array_equal(logp2.cpu().numpy().view(np.uint32), lp.view(np.uint32))
+
+
 def _invariance(model, sp, tok, W):
     """Bitwise: repeat, suffix change, batch composition, shorter window."""
     import torch

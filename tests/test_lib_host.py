@@ -1,6 +1,7 @@
 """Host-side checks of liblmgc that need no GPU: the library loads and exports
 every entry point of include/lmgc.h; its manifest, token counts, arithmetic
 coder, deserialiser and container parser agree with the oracle."""
+import dataclasses
 import os
 import re
 
@@ -151,6 +152,24 @@ def test_library_reads_two_token_separator_container():
     bad[27] = 18                     # bin count of a one-token alphabet with a second id
     with pytest.raises(B.LMGCError):
         B.container_info(bytes(bad))
+
+
+def test_library_renorm_flag():
+    """Table mode: validated in the parameters, stored at header offset 120."""
+    sp = B.serial_params(hex_serial(window=8, bos_id=1))
+    sp.renorm = 2
+    with pytest.raises(B.LMGCError) as e:
+        B.alphabet_size(sp)
+    assert e.value.code == -1
+    ser = dataclasses.replace(hex_serial(window=8, bos_id=1), renorm=1)
+    buf = opipe.pack_container(ser, 2, 1, 1 << 16, [3, 4, 5], [b"\x01", b"\x02", b"\x03"])
+    assert int.from_bytes(buf[120:124], "little") == 1
+    assert B.container_info(buf)["n_windows"] == 3
+    bad = bytearray(buf)
+    bad[120] = 2
+    with pytest.raises(B.LMGCError) as e:
+        B.container_info(bytes(bad))
+    assert e.value.code == -5
 
 
 def test_container_info_and_corruption():
