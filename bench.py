@@ -93,6 +93,23 @@ def load_traffic(path):
     return tj.get("bytes_per_launch")
 
 
+def describe_model(m):
+    if m.arch == "gpt2":
+        return f"GPT-2-shape decoder ({m.n_layers} layers, d={m.d_model}, vocab {m.vocab}, {m.dtype})"
+    size = "Llama-2-7B-shape" if m.d_model == 4096 else "Llama-style"
+    return (f"{size} decoder ({m.n_layers} layers, d={m.d_model}, {m.n_heads}/{m.n_kv_heads} heads, "
+            f"SwiGLU {m.d_ff}, vocab {m.vocab}, {m.dtype})")
+
+
+def describe_serial(s, tok_per_value):
+    sep = "".join(chr(c) for c in (s.sep_id, s.sep2_id) if c >= 0)
+    group = "no separator" if s.bytes_per_group == 0 else \
+        f"separator {sep!r} after every {s.bytes_per_group} bytes"
+    tables = "tables renormalised over the alphabet" if getattr(s, "renorm", 0) else \
+        "full-vocabulary tables"
+    return f"{s.bytes_per_value}-byte values as hex digits, {group} ({tok_per_value:g} tokens per value), {tables}"
+
+
 def copy_calibration(mib):
     """Plain device-to-device copies of a known size, for scaling the HBM
     byte counters (run under the profiler's counter collection)."""
@@ -112,6 +129,11 @@ def main():
     ap.add_argument("--steps", type=int, default=12)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="7b")
+    ap.add_argument("--separator", default=None,
+                    help="serialisation variant of Sec. 5.2: H_s (default), H_c, H_semi, H_c+s")
+    ap.add_argument("--bpg", type=int, default=None, help="bytes per separator group (0 = H_n)")
+    ap.add_argument("--renorm", action="store_true",
+                    help="tables renormalised over the alphabet (LM head cut to the alphabet)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-values", type=int, default=2)
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_gemm_up_7b.json"))
@@ -129,11 +151,23 @@ def main():
     import numpy as np
     import torch
 
+    import dataclasses
+
     from paper_2409_17836_amd import binding as B
-    from synth import get_workload
+    from synth import get_workload, parse_lossy
+    from synth.configs import SEPARATORS
     from synth.gen import iter_weights, workload_values
 
     w = get_workload(args.workload)
+    serial = w.serial
+    if args.separator:
+        sep, sep2 = SEPARATORS[args.separator]
+        serial = dataclasses.replace(serial, sep_id=sep, sep2_id=sep2)
+    if args.bpg is not None:
+        serial = dataclasses.replace(serial, bytes_per_group=args.bpg)
+    if args.renorm:
+        serial = dataclasses.replace(serial, renorm=1)
+    w = w.with_(serial=serial)
     Bw, W = w.batch, w.serial.window
     dev = torch.device("cuda:0")
     log(f"[bench] workload {w.name}: generating {w.n_values} values and weights")
@@ -151,10 +185,21 @@ def main():
     torch.cuda.empty_cache()
     sp = B.serial_params(w.serial)
     dv = torch.from_numpy(values).to(dev)
-    n_win = B.num_windows(w.n_values, sp)
+    lossy_ms = None
+    if w.lossy:
+        # Sec. 5.4: the lossy steps run once over the whole vector on the GPU;
+        # the timed steps compress their output, resident in HBM
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        dv = B.lossy_prepare(dv, parse_lossy(w.lossy))
+        torch.cuda.synchronize()
+        lossy_ms = (time.perf_counter() - t0) * 1e3
+        log(f"[bench] lossy steps {w.lossy}: {lossy_ms:.2f} ms for {w.n_values} values")
+    n_vals = dv.numel()
+    n_win = B.num_windows(n_vals, sp)
     need = (args.warmup + args.steps) * Bw
     assert need <= n_win, f"{need} windows needed, workload has {n_win}"
-    ws = B.workspace(model.codec_workspace(w.n_values, sp, Bw))
+    ws = B.workspace(model.codec_workspace(n_vals, sp, Bw))
     stream = torch.cuda.current_stream()
     log(f"[bench] model ready; warmup {args.warmup} step(s)")
 
@@ -173,9 +218,10 @@ def main():
     kern = {k: B.timing_read(k) for k in B.KINDS}
     B.timing_enable(False)
 
-    n_tok = B.num_tokens(w.n_values, sp)
+    n_tok = B.num_tokens(n_vals, sp)
     tok_done = min(n_tok, (args.warmup + args.steps) * Bw * W) - args.warmup * Bw * W
-    grad_bytes = tok_done / B.num_tokens(1, sp) * w.serial.bytes_per_value
+    tok_per_value = n_tok / max(n_vals, 1)
+    grad_bytes = tok_done / tok_per_value * w.serial.bytes_per_value
     value = grad_bytes / dt / 1e6
     ms_step = dt * 1e3 / args.steps
 
@@ -204,12 +250,13 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded Laplace gradients, random-init weights)",
         "config": {
-            "workload": f"{w.name}: Llama-2-7B-shape decoder, float32 gradients ~ {w.dist}, "
-                        f"8 hex digits + separator per value",
+            "workload": f"{w.name}: {describe_model(w.model)}, gradients ~ {w.dist}"
+                        + (f" then {w.lossy}" if w.lossy else "")
+                        + f", {describe_serial(w.serial, tok_per_value)}",
             "windows_per_step": Bw,
             "window_tokens": W,
             "tokens_per_step": Bw * W,
-            "values_per_step": round(Bw * W / 9, 1),
+            "values_per_step": round(Bw * W / tok_per_value, 1),
             "parallelism": "single GPU",
         },
         "tokens_per_s": round(tok_done / dt, 1),
@@ -230,7 +277,9 @@ def main():
             "flop_per_launch": flop_launch,
         },
     }
-    if not args.no_cpu_baseline:
+    if lossy_ms is not None:
+        out["lossy_prep_ms"] = round(lossy_ms, 3)
+    if not args.no_cpu_baseline and not w.lossy:
         log("[bench] timing the CPU oracle on a bounded sample")
         cb = cpu_baseline(w, host, values, args.cpu_sample_values)
         out["cpu_baseline"] = {k: v for k, v in cb.items() if k != "seconds"}
