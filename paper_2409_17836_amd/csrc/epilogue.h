@@ -48,7 +48,20 @@ __device__ inline float silu_f(float x) {
 
 __device__ inline float gelu_tanh_f(float x) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  return 0.5f * x * (1.0f + tanhf(k0 * (x + 0.044715f * x * x * x)));
+  const float inner = __builtin_fmaf(0.044715f * x * x, x, x);  // explicit fusion, as in rope_rot
+  return 0.5f * x * (1.0f + tanhf(k0 * inner));
+}
+
+// The per-element arithmetic of the residual add and the RoPE rotation, in
+// one place: the tiled and the one-row kernels must give the same bits.
+// Products that meet an addition are fused explicitly: left to the
+// compiler, a sum of two products may be contracted around either product
+// depending on the surrounding code, which changes the rounding between
+// the two kernels.
+__device__ inline float resid_add(float old, float v, float bias) { return old + (v + bias); }
+__device__ inline void rope_rot(float vlo, float vhi, float c, float s, float& lo, float& hi) {
+  lo = __builtin_fmaf(vlo, c, -(vhi * s));
+  hi = __builtin_fmaf(vhi, c, vlo * s);
 }
 
 // Column info of one (col, col + 32) pair.
@@ -112,7 +125,12 @@ struct Epi {
 
   __device__ static inline void row(const EpiArgs& e, const ColInfo& c, int col, int rw, int b,
                                     int pos, float vlo, float vhi) {
-    if (!c.valid) return;
+    if (c.valid) row_in(e, c, col, rw, b, pos, vlo, vhi);
+  }
+
+  // row() for a column known to be valid
+  __device__ static inline void row_in(const EpiArgs& e, const ColInfo& c, int col, int rw, int b,
+                                       int pos, float vlo, float vhi) {
     const int h = hdim(e);
     if (KIND == EPI_STORE_F32) {
       float* p = e.c + (int64_t)rw * e.ldc;
@@ -120,8 +138,8 @@ struct Epi {
       if (col + 32 < e.N) p[col + 32] = vhi;
     } else if (KIND == EPI_RESID) {
       float* p = e.c + (int64_t)rw * e.ldc;
-      p[col] += vlo + c.blo;
-      p[col + 32] += vhi + c.bhi;
+      p[col] = resid_add(p[col], vlo, c.blo);
+      p[col + 32] = resid_add(p[col + 32], vhi, c.bhi);
     } else if (KIND == EPI_SWIGLU) {
       const int f = (col >> 6) * 32 + (col & 31);
       store_act<T>(e.out, (int64_t)rw * e.ld_out + f, silu_f(vlo) * vhi);
@@ -132,13 +150,7 @@ struct Epi {
     } else if (KIND == EPI_QKV_ROPE) {
       if (c.seg < 2) {
         const float2 cs = e.rope[pos * (h / 2) + c.i];
-        const float lo = vlo * cs.x - vhi * cs.y;
-        const float hi = vhi * cs.x + vlo * cs.y;
-        const int H = c.seg == 0 ? e.Hq : e.Hkv;
-        void* dst = c.seg == 0 ? e.q : e.k;
-        const int64_t base = (((int64_t)b * H + c.head) * e.W + pos) * h;
-        store_act<T>(dst, base + c.i, lo);
-        store_act<T>(dst, base + c.i + h / 2, hi);
+        store_qk(e, c, b, pos, vlo, vhi, cs.x, cs.y);
       } else {
         store_act<T>(e.v, vidx(e, b, e.Hkv, c.head, c.i, pos), vlo);
         store_act<T>(e.v, vidx(e, b, e.Hkv, c.head2, c.i2, pos), vhi);
@@ -159,12 +171,68 @@ struct Epi {
                           : (((int64_t)b * H + head) * e.W + pos) * h + i;
   }
 
-  // Rows rw0 .. rw0+3 (positions p0 .. p0+3 of window b; p0 % 4 == 0).
+  // What the epilogue of rows rw0 .. rw0+3 reads before it writes: the
+  // residual values (RESID) or the RoPE cos/sin of the q/k rotation
+  // (QKV_ROPE).  A load cannot move above an earlier store that may alias
+  // it, so the tiled kernel issues these loads for its next row block before
+  // the stores of the current one.
+  struct Pre4 {
+    float x[4], y[4];
+  };
+  // FULL: the caller knows every row and column of its tile is in range.
+  template <bool FULL>
+  __device__ static inline Pre4 pre4(const EpiArgs& e, const ColInfo& c, int col, int rw0, int M, int p0) {
+    Pre4 q;
+#pragma unroll
+    for (int r = 0; r < 4; r++) q.x[r] = q.y[r] = 0.f;
+    if (!FULL && !c.valid) return q;
+    if (KIND == EPI_RESID) {
+#pragma unroll
+      for (int r = 0; r < 4; r++)
+        if (FULL || rw0 + r < M) {
+          const float* p = e.c + (int64_t)(rw0 + r) * e.ldc;
+          q.x[r] = p[col];
+          q.y[r] = p[col + 32];
+        }
+    } else if (KIND == EPI_QKV_ROPE) {
+      if (c.seg < 2) {
+        const int h = hdim(e);
+#pragma unroll
+        for (int r = 0; r < 4; r++)
+          if (FULL || rw0 + r < M) {
+            const float2 cs = e.rope[(p0 + r) * (h / 2) + c.i];
+            q.x[r] = cs.x;
+            q.y[r] = cs.y;
+          }
+      }
+    }
+    return q;
+  }
+
+  // Rows rw0 .. rw0+3 (positions p0 .. p0+3 of window b; p0 % 4 == 0), with
+  // the values pre4 loaded for them.
+  template <bool FULL>
   __device__ static inline void rows4(const EpiArgs& e, const ColInfo& c, int col, int rw0, int M,
-                                      int b, int p0, const float* lo, const float* hi) {
-    if (!c.valid) return;
+                                      int b, int p0, const float* lo, const float* hi, const Pre4& q) {
+    if (!FULL && !c.valid) return;
+    if (KIND == EPI_RESID) {
+#pragma unroll
+      for (int r = 0; r < 4; r++)
+        if (FULL || rw0 + r < M) {
+          float* p = e.c + (int64_t)(rw0 + r) * e.ldc;
+          p[col] = resid_add(q.x[r], lo[r], c.blo);
+          p[col + 32] = resid_add(q.y[r], hi[r], c.bhi);
+        }
+      return;
+    }
+    if (KIND == EPI_QKV_ROPE && c.seg < 2) {
+#pragma unroll
+      for (int r = 0; r < 4; r++)
+        if (FULL || rw0 + r < M) store_qk(e, c, b, p0 + r, lo[r], hi[r], q.x[r], q.y[r]);
+      return;
+    }
     constexpr bool qkv = KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS;
-    if (qkv && sizeof(T) == 2 && rw0 + 3 < M && (c.seg == 2 || c.seg2 == 2)) {
+    if (qkv && sizeof(T) == 2 && (FULL || rw0 + 3 < M) && (c.seg == 2 || c.seg2 == 2)) {
       const int H = KIND == EPI_QKV_ROPE ? e.Hkv : e.Hq;
       const float bl = KIND == EPI_QKV_BIAS ? c.blo : 0.f, bh = KIND == EPI_QKV_BIAS ? c.bhi : 0.f;
       if (c.seg == 2) {
@@ -181,10 +249,22 @@ struct Epi {
     }
 #pragma unroll
     for (int r = 0; r < 4; r++)
-      if (rw0 + r < M) row(e, c, col, rw0 + r, b, p0 + r, lo[r], hi[r]);
+      if (FULL || rw0 + r < M) row_in(e, c, col, rw0 + r, b, p0 + r, lo[r], hi[r]);
   }
 
  private:
+  // RoPE-rotated q or k pair (dims i and i + hd/2 of the head) of one row
+  __device__ static inline void store_qk(const EpiArgs& e, const ColInfo& c, int b, int pos, float vlo,
+                                         float vhi, float cs, float sn) {
+    const int h = hdim(e);
+    float lo, hi;
+    rope_rot(vlo, vhi, cs, sn, lo, hi);
+    const int H = c.seg == 0 ? e.Hq : e.Hkv;
+    void* dst = c.seg == 0 ? e.q : e.k;
+    const int64_t base = (((int64_t)b * H + c.head) * e.W + pos) * h;
+    store_act<T>(dst, base + c.i, lo);
+    store_act<T>(dst, base + c.i + h / 2, hi);
+  }
   // four consecutive bf16 values, 8-byte aligned
   __device__ static inline void store4(void* p, int64_t idx, float a, float b, float c, float d) {
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));

@@ -211,21 +211,42 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   // 4 (lane >> 4) + r, r = 0..3.  Blocks j and j + 2 give the column pair
   // (col, col + 32).  Rows 4 (lane >> 4) + 0..3 never straddle a window
   // (W is a multiple of 8).
+  // The reads an epilogue needs (residual, RoPE table) for row block i + 1
+  // are issued before the stores of block i.  Whole tiles (all but the
+  // ragged edges) take a path without row and column checks, so the
+  // epilogue stays one basic block.
   using E = Epi<uint16_t, KIND, HD>;
+  using Pre4 = typename E::Pre4;
   const int c0 = n0 + wn * 64 + (lane & 15);
   const ColInfo ci0 = E::column(e, c0), ci1 = E::column(e, c0 + 16);
   const int W = e.W > 0 ? e.W : 1;
+  auto epilogue = [&](auto full_tag) __attribute__((always_inline)) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    const int rb = m0 + wm * 128 + 4 * kq;
+    Pre4 q0 = E::template pre4<FULL>(e, ci0, c0, rb, M, rb % W);
+    Pre4 q1 = E::template pre4<FULL>(e, ci1, c0 + 16, rb, M, rb % W);
 #pragma unroll
-  for (int i = 0; i < 8; i++) {
-    const int r0 = m0 + wm * 128 + 16 * i + 4 * kq;
-    const int b = r0 / W, p0 = r0 - b * W;
-    const float a0[4] = {acc[i][0][0], acc[i][0][1], acc[i][0][2], acc[i][0][3]};
-    const float a2[4] = {acc[i][2][0], acc[i][2][1], acc[i][2][2], acc[i][2][3]};
-    const float a1[4] = {acc[i][1][0], acc[i][1][1], acc[i][1][2], acc[i][1][3]};
-    const float a3[4] = {acc[i][3][0], acc[i][3][1], acc[i][3][2], acc[i][3][3]};
-    E::rows4(e, ci0, c0, r0, M, b, p0, a0, a2);
-    E::rows4(e, ci1, c0 + 16, r0, M, b, p0, a1, a3);
-  }
+    for (int i = 0; i < 8; i++) {
+      const int r0 = rb + 16 * i;
+      const int b = r0 / W, p0 = r0 - b * W;
+      Pre4 n0q = q0, n1q = q1;
+      if (i + 1 < 8) {
+        const int r1 = r0 + 16, p1 = r1 % W;
+        n0q = E::template pre4<FULL>(e, ci0, c0, r1, M, p1);
+        n1q = E::template pre4<FULL>(e, ci1, c0 + 16, r1, M, p1);
+      }
+      const float a0[4] = {acc[i][0][0], acc[i][0][1], acc[i][0][2], acc[i][0][3]};
+      const float a2[4] = {acc[i][2][0], acc[i][2][1], acc[i][2][2], acc[i][2][3]};
+      const float a1[4] = {acc[i][1][0], acc[i][1][1], acc[i][1][2], acc[i][1][3]};
+      const float a3[4] = {acc[i][3][0], acc[i][3][1], acc[i][3][2], acc[i][3][3]};
+      E::template rows4<FULL>(e, ci0, c0, r0, M, b, p0, a0, a2, q0);
+      E::template rows4<FULL>(e, ci1, c0 + 16, r0, M, b, p0, a1, a3, q1);
+      q0 = n0q;
+      q1 = n1q;
+    }
+  };
+  if (m0 + BM <= M && n0 + BN <= e.N) epilogue(std::true_type{});
+  else epilogue(std::false_type{});
 }
 
 // Decoding step (M <= 16 rows: one row per window).  A workgroup of four
