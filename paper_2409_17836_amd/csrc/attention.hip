@@ -86,9 +86,24 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   __shared__ u32x4 sV0[HD * 8], sV1[HD * 8];  // V^T: [dim][64 keys]
 
   const int nqb = (W + BQ - 1) / BQ;
-  // longest blocks first; a decoding step (dq >= 0) runs only dq's block
-  const int qb = dq >= 0 ? dq / BQ : nqb - 1 - (int)blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  int qb, h;
+  const int b = blockIdx.z;
+  if (dq >= 0) {
+    // a decoding step runs only the block of position dq
+    qb = dq / BQ;
+    h = blockIdx.y;
+  } else {
+    // Workgroup x of window b runs on XCD x % 8 (gridDim.x is a multiple of
+    // 8).  Each XCD gets a contiguous range of the window's (head, query
+    // block) items, so all blocks of a head read its K and V through one L2
+    // (spread over the eight L2s, the K/V tiles came from HBM); within a head
+    // the longest blocks go first.
+    const int per = gridDim.x / 8;
+    const int t = ((int)blockIdx.x % 8) * per + (int)blockIdx.x / 8;
+    if (t >= nqb * Hq) return;
+    h = t / nqb;
+    qb = nqb - 1 - (t - h * nqb);
+  }
   const int kvh = h * Hkv / Hq;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -393,7 +408,8 @@ hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uin
                                  hipStream_t s) {
   if (B <= 0 || W <= 0) return hipSuccess;
   if (W % 8 || dq >= W) return hipErrorInvalidValue;
-  const dim3 grid(dq >= 0 ? 1 : (W + 127) / 128, Hq, B), block(256);
+  const int items = (W + 127) / 128 * Hq;  // (head, 128-query block) items per window
+  const dim3 grid = dq >= 0 ? dim3(1, Hq, B) : dim3((items + 7) / 8 * 8, 1, B), block(256);
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)hd));
   if (hd == 128)
     hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);

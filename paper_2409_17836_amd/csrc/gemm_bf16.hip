@@ -218,7 +218,21 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   using E = Epi<uint16_t, KIND, HD>;
   using Pre4 = typename E::Pre4;
   const int c0 = n0 + wn * 64 + (lane & 15);
-  const ColInfo ci0 = E::column(e, c0), ci1 = E::column(e, c0 + 16);
+  ColInfo ci0 = E::column(e, c0), ci1 = E::column(e, c0 + 16);
+  if (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS) {
+    // bf16 models have head_dim 64 or 128, so q, k and v and every head are
+    // whole 64-column groups: a wave's columns share segment and head.
+    // Saying so turns the epilogue's q/k/v branches into scalar ones.
+    auto uniform = [](ColInfo& c) __attribute__((always_inline)) {
+      c.valid = __builtin_amdgcn_readfirstlane((int)c.valid) != 0;
+      c.seg = __builtin_amdgcn_readfirstlane(c.seg);
+      c.seg2 = __builtin_amdgcn_readfirstlane(c.seg2);
+      c.head = __builtin_amdgcn_readfirstlane(c.head);
+      c.head2 = __builtin_amdgcn_readfirstlane(c.head2);
+    };
+    uniform(ci0);
+    uniform(ci1);
+  }
   const int W = e.W > 0 ? e.W : 1;
   auto epilogue = [&](auto full_tag) __attribute__((always_inline)) {
     constexpr bool FULL = decltype(full_tag)::value;
