@@ -234,8 +234,54 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     uniform(ci1);
   }
   const int W = e.W > 0 ? e.W : 1;
+  // V columns of a whole tile (bf16 QKV): the wave's 128 rows x 64 columns
+  // go through LDS, transposed, so that each V^T row (a dim of a head) is
+  // written as 16-byte pieces of 8 consecutive positions.  A wave's region
+  // is 16 KB: 64 rows (columns) of 128 positions, 16-byte chunks swizzled by
+  // chunk ^ (row & 15).  Needs W % 128 == 0 so the rows lie in one window.
+  auto v_transposed = [&]() __attribute__((always_inline)) {
+    u32x4* reg = (wave < 2 ? sA0 : wave < 4 ? sA1 : wave < 6 ? sA2 : sB0) + (wave & 1) * 1024;
+    char* regb = reinterpret_cast<char*>(reg);
+    const float bl0 = KIND == EPI_QKV_BIAS ? ci0.blo : 0.f, bh0 = KIND == EPI_QKV_BIAS ? ci0.bhi : 0.f;
+    const float bl1 = KIND == EPI_QKV_BIAS ? ci1.blo : 0.f, bh1 = KIND == EPI_QKV_BIAS ? ci1.bhi : 0.f;
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int i = 0; i < 8; i++)
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const int kap = (lane & 15) + 16 * j, rho = 16 * i + 4 * kq;
+        const float bias = j == 0 ? bl0 : j == 1 ? bl1 : j == 2 ? bh0 : bh1;
+        const bf16x4 val = {(__bf16)(acc[i][j][0] + bias), (__bf16)(acc[i][j][1] + bias),
+                            (__bf16)(acc[i][j][2] + bias), (__bf16)(acc[i][j][3] + bias)};
+        const int off = kap * 256 + (((rho >> 3) ^ (kap & 15)) << 4) + (rho & 7) * 2;
+        *reinterpret_cast<bf16x4*>(regb + off) = val;
+      }
+    const int H = KIND == EPI_QKV_ROPE ? e.Hkv : e.Hq;
+    const int h = HD ? HD : e.hd;
+    const int row0 = m0 + wm * 128, b = row0 / W, pos0 = row0 - b * W;
+    // first V column: after q and k (Hq and Hkv heads for RoPE models,
+    // Hq and Hq for GPT-2's fused projection)
+    const int vcol0 = n0 + wn * 64 - (KIND == EPI_QKV_ROPE ? e.Hq + e.Hkv : 2 * e.Hq) * h;
+#pragma unroll
+    for (int t = 0; t < 16; t++) {
+      const int c = lane + 64 * t, kap = c >> 4, ch = c & 15;
+      const u32x4 val = reg[kap * 16 + (ch ^ (kap & 15))];
+      const int cc = vcol0 + kap, head = cc / h, dim = cc - head * h;
+      uint16_t* dst = (uint16_t*)e.v + (((int64_t)b * H + head) * h + dim) * W + pos0 + ch * 8;
+      *reinterpret_cast<u32x4*>(dst) = val;
+    }
+  };
   auto epilogue = [&](auto full_tag) __attribute__((always_inline)) {
     constexpr bool FULL = decltype(full_tag)::value;
+    if constexpr (FULL && (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS)) {
+      if (W % 128 == 0) {
+        barrier();  // every wave has finished reading the operand buffers
+        if (ci0.seg == 2) {
+          v_transposed();
+          return;
+        }
+      }
+    }
     const int rb = m0 + wm * 128 + 4 * kq;
     Pre4 q0 = E::template pre4<FULL>(e, ci0, c0, rb, M, rb % W);
     Pre4 q1 = E::template pre4<FULL>(e, ci1, c0 + 16, rb, M, rb % W);
