@@ -8,9 +8,14 @@
 // wn*64 .. +64 as 8 x 4 blocks of v_mfma_f32_16x16x32_bf16.
 //
 // Operand pipeline.  K advances in stages of 64.  Stages go to LDS with
-// buffer loads straight into LDS (no staging registers): A through a ring of
-// three 32 KB buffers, loaded two stages ahead, B through two, loaded one
-// stage ahead (5 x 32 KB = the whole 160 KB LDS).  A wave's eight loads of a
+// buffer loads straight into LDS (no staging registers): one operand through
+// a ring of three 32 KB buffers, loaded two stages ahead, the other through
+// two, loaded one stage ahead (5 x 32 KB = the whole 160 KB LDS).  The ring
+// holds A by default and B when RB is set: the deeper prefetch goes to the
+// operand whose panels miss L2 more often.  A wide weight matrix (N >= 2K:
+// gate/up, QKV, LM head) has new B panels for every wave of tiles, while an
+// XCD's A panels repeat; for a narrow one (the N = d products that add into
+// the residual) B stays cached and A streams.  A wave's eight loads of a
 // stage are spread through its MFMA stream (one after every four MFMAs)
 // instead of being issued in one burst after the barrier: all workgroups
 // bursting at once queue in L2 and roughly double the load latency.  Each
@@ -76,12 +81,13 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
 }
 
-template <int KIND, int HD>
+template <int KIND, int HD, bool RB>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Bw, int M, int K, int ntm,
     int ntn, EpiArgs e) {
-  __shared__ u32x4 sA0[BM * 8], sA1[BM * 8], sA2[BM * 8];  // 3 x 32 KB
-  __shared__ u32x4 sB0[BN * 8], sB1[BN * 8];               // 2 x 32 KB
+  // sR*: the ring of three (A, or B if RB); sD*: the double buffer
+  __shared__ u32x4 sR0[BM * 8], sR1[BM * 8], sR2[BM * 8];  // 3 x 32 KB
+  __shared__ u32x4 sD0[BN * 8], sD1[BN * 8];               // 2 x 32 KB
 
   int tm, tn;
   if (!map_tile(blockIdx.x, gridDim.x, ntm, ntn, tm, tn)) return;
@@ -124,10 +130,21 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(sb + (wave * 4 + i) * 64), 16, voff[i],
                                              k0 * 2, 0, 0);
   };
-  // One stage from (sa, sb).  B of stage kb goes to nb and A of stage ka to na
+  // One stage from ring buffer sr and double buffer sd.  The double-buffered
+  // operand of stage kd goes to nd and the ring operand of stage kr to nr
   // (negative: no load), one load after every kLoadEvery MFMAs.
-  auto compute = [&](const u32x4* sa, const u32x4* sb, u32x4* na, int ka, u32x4* nb, int kb)
+  auto ld_r = [&](u32x4* buf, int i, int k0) __attribute__((always_inline)) {
+    if (RB) ldB(buf, i, k0);
+    else ldA(buf, i, k0);
+  };
+  auto ld_d = [&](u32x4* buf, int i, int k0) __attribute__((always_inline)) {
+    if (RB) ldA(buf, i, k0);
+    else ldB(buf, i, k0);
+  };
+  auto compute = [&](const u32x4* sr, const u32x4* sd, u32x4* nr, int kr, u32x4* nd, int kd)
       __attribute__((always_inline)) {
+    const u32x4* sa = RB ? sd : sr;
+    const u32x4* sb = RB ? sr : sd;
     int issued = 0, nm = 0;
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ks++) {
@@ -145,9 +162,9 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
           if (++nm % kLoadEvery == 0 && issued < 8) {
             __builtin_amdgcn_sched_barrier(0);
             if (issued < 4) {
-              if (kb >= 0) ldB(nb, issued, kb);
+              if (kd >= 0) ld_d(nd, issued, kd);
             } else {
-              if (ka >= 0) ldA(na, issued - 4, ka);
+              if (kr >= 0) ld_r(nr, issued - 4, kr);
             }
             __builtin_amdgcn_sched_barrier(0);
             issued++;
@@ -161,51 +178,51 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  // Stage t reads A buffer t % 3 and B buffer t % 2.  During stage t a wave
-  // loads B(t+1) (into the B buffer stage t-1 used) and A(t+2) (into the A
-  // buffer of stage t-1), in that order; at the start of stage t its loads in
-  // flight are, oldest first, A(t), B(t), A(t+1), so vmcnt(4) leaves only
-  // A(t+1) outstanding.  The barrier then makes every wave's part of stage t
-  // visible, and ends every wave's reads of stage t-1.
-  auto full = [&](int t, const u32x4* ca, const u32x4* cb, u32x4* nb, u32x4* na)
+  // Stage t reads ring buffer t % 3 and double buffer t % 2.  During stage t
+  // a wave loads D(t+1) (into the double buffer stage t-1 used) and R(t+2)
+  // (into the ring buffer of stage t-1), in that order; at the start of stage
+  // t its loads in flight are, oldest first, R(t), D(t), R(t+1), so vmcnt(4)
+  // leaves only R(t+1) outstanding.  The barrier then makes every wave's part
+  // of stage t visible, and ends every wave's reads of stage t-1.
+  auto full = [&](int t, const u32x4* cr, const u32x4* cd, u32x4* nd, u32x4* nr)
       __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(kVmcnt4);
     barrier();
-    compute(ca, cb, na, (t + 2) * BK, nb, (t + 1) * BK);
+    compute(cr, cd, nr, (t + 2) * BK, nd, (t + 1) * BK);
   };
   const int nk = K / BK;
-  auto tail = [&](int t, const u32x4* ca, const u32x4* cb, u32x4* nb, u32x4* na)
+  auto tail = [&](int t, const u32x4* cr, const u32x4* cd, u32x4* nd, u32x4* nr)
       __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(kVmcnt0);
     barrier();
-    compute(ca, cb, na, t + 2 < nk ? (t + 2) * BK : -1, nb, t + 1 < nk ? (t + 1) * BK : -1);
+    compute(cr, cd, nr, t + 2 < nk ? (t + 2) * BK : -1, nd, t + 1 < nk ? (t + 1) * BK : -1);
   };
 #pragma unroll
-  for (int i = 0; i < 4; i++) ldA(sA0, i, 0);
+  for (int i = 0; i < 4; i++) ld_r(sR0, i, 0);
 #pragma unroll
-  for (int i = 0; i < 4; i++) ldB(sB0, i, 0);
+  for (int i = 0; i < 4; i++) ld_d(sD0, i, 0);
   if (nk > 1) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) ldA(sA1, i, BK);
+    for (int i = 0; i < 4; i++) ld_r(sR1, i, BK);
   }
   // buffers repeat every 6 stages; the loop runs while all six steps and the
   // loads they issue are in range, the rest (at most 7 stages) is predicated
   int t = 0;
   for (; t + 8 <= nk; t += 6) {
-    full(t + 0, sA0, sB0, sB1, sA2);
-    full(t + 1, sA1, sB1, sB0, sA0);
-    full(t + 2, sA2, sB0, sB1, sA1);
-    full(t + 3, sA0, sB1, sB0, sA2);
-    full(t + 4, sA1, sB0, sB1, sA0);
-    full(t + 5, sA2, sB1, sB0, sA1);
+    full(t + 0, sR0, sD0, sD1, sR2);
+    full(t + 1, sR1, sD1, sD0, sR0);
+    full(t + 2, sR2, sD0, sD1, sR1);
+    full(t + 3, sR0, sD1, sD0, sR2);
+    full(t + 4, sR1, sD0, sD1, sR0);
+    full(t + 5, sR2, sD1, sD0, sR1);
   }
-  if (t + 0 < nk) tail(t + 0, sA0, sB0, sB1, sA2);
-  if (t + 1 < nk) tail(t + 1, sA1, sB1, sB0, sA0);
-  if (t + 2 < nk) tail(t + 2, sA2, sB0, sB1, sA1);
-  if (t + 3 < nk) tail(t + 3, sA0, sB1, sB0, sA2);
-  if (t + 4 < nk) tail(t + 4, sA1, sB0, sB1, sA0);
-  if (t + 5 < nk) tail(t + 5, sA2, sB1, sB0, sA1);
-  if (t + 6 < nk) tail(t + 6, sA0, sB0, sB1, sA2);
+  if (t + 0 < nk) tail(t + 0, sR0, sD0, sD1, sR2);
+  if (t + 1 < nk) tail(t + 1, sR1, sD1, sD0, sR0);
+  if (t + 2 < nk) tail(t + 2, sR2, sD0, sD1, sR1);
+  if (t + 3 < nk) tail(t + 3, sR0, sD1, sD0, sR2);
+  if (t + 4 < nk) tail(t + 4, sR1, sD0, sD1, sR0);
+  if (t + 5 < nk) tail(t + 5, sR2, sD1, sD0, sR1);
+  if (t + 6 < nk) tail(t + 6, sR0, sD0, sD1, sR2);
 
   // Epilogue.  16 x 16 block layout: lane holds column (lane & 15) and rows
   // 4 (lane >> 4) + r, r = 0..3.  Blocks j and j + 2 give the column pair
@@ -240,7 +257,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   // is 16 KB: 64 rows (columns) of 128 positions, 16-byte chunks swizzled by
   // chunk ^ (row & 15).  Needs W % 128 == 0 so the rows lie in one window.
   auto v_transposed = [&]() __attribute__((always_inline)) {
-    u32x4* reg = (wave < 2 ? sA0 : wave < 4 ? sA1 : wave < 6 ? sA2 : sB0) + (wave & 1) * 1024;
+    u32x4* reg = (wave < 2 ? sR0 : wave < 4 ? sR1 : wave < 6 ? sR2 : sD0) + (wave & 1) * 1024;
     char* regb = reinterpret_cast<char*>(reg);
     const float bl0 = KIND == EPI_QKV_BIAS ? ci0.blo : 0.f, bh0 = KIND == EPI_QKV_BIAS ? ci0.bhi : 0.f;
     const float bl1 = KIND == EPI_QKV_BIAS ? ci1.blo : 0.f, bh1 = KIND == EPI_QKV_BIAS ? ci1.bhi : 0.f;
@@ -415,34 +432,51 @@ hipError_t launch_rows_kind(const uint16_t* A, const uint16_t* B, int M, int N_p
   return hipGetLastError();
 }
 
+template <int KIND, int HD>
+hipError_t launch_one(const uint16_t* A, const uint16_t* B, int M, int K, int ntm, int ntn, bool rb,
+                      const EpiArgs& e, hipStream_t s) {
+  const int total = ntm * ntn;
+  const dim3 grid((total + kXcds - 1) / kXcds * kXcds), block(kThreads);
+  if constexpr (KIND == EPI_RESID) {
+    (void)rb;  // the residual products (N = d) keep the ring on A
+    hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, false>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
+  } else {
+    if (rb)
+      hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, true>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
+    else
+      hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, false>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
+  }
+  return hipGetLastError();
+}
+
+// HD != 0: the QKV kinds of a bf16 model with that head dim; HD == 0: the rest.
 template <int HD>
 hipError_t launch_kind(const uint16_t* A, const uint16_t* B, int M, int K, int ntm, int ntn,
                        const EpiArgs& e, hipStream_t s) {
-  const int total = ntm * ntn;
-  const dim3 grid((total + kXcds - 1) / kXcds * kXcds), block(kThreads);
-  switch (e.kind) {
-    case EPI_STORE_F32:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE_F32, HD>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
-      break;
-    case EPI_RESID:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_RESID, HD>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
-      break;
-    case EPI_QKV_ROPE:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV_ROPE, HD>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
-      break;
-    case EPI_QKV_BIAS:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV_BIAS, HD>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
-      break;
-    case EPI_SWIGLU:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, HD>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
-      break;
-    case EPI_BIAS_GELU:
-      hipLaunchKernelGGL((gemm_bf16_kernel<EPI_BIAS_GELU, HD>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
-      break;
-    default:
-      return hipErrorInvalidValue;
+  const bool rb = (int64_t)ntn * BN >= 2 * (int64_t)K;  // wide weight matrix: the ring holds B
+  if constexpr (HD != 0) {
+    switch (e.kind) {
+      case EPI_QKV_ROPE:
+        return launch_one<EPI_QKV_ROPE, HD>(A, B, M, K, ntm, ntn, rb, e, s);
+      case EPI_QKV_BIAS:
+        return launch_one<EPI_QKV_BIAS, HD>(A, B, M, K, ntm, ntn, rb, e, s);
+      default:
+        return hipErrorInvalidValue;
+    }
+  } else {
+    switch (e.kind) {
+      case EPI_STORE_F32:
+        return launch_one<EPI_STORE_F32, 0>(A, B, M, K, ntm, ntn, rb, e, s);
+      case EPI_RESID:
+        return launch_one<EPI_RESID, 0>(A, B, M, K, ntm, ntn, rb, e, s);
+      case EPI_SWIGLU:
+        return launch_one<EPI_SWIGLU, 0>(A, B, M, K, ntm, ntn, rb, e, s);
+      case EPI_BIAS_GELU:
+        return launch_one<EPI_BIAS_GELU, 0>(A, B, M, K, ntm, ntn, rb, e, s);
+      default:
+        return hipErrorInvalidValue;
+    }
   }
-  return hipGetLastError();
 }
 
 }  // namespace
