@@ -326,25 +326,35 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   else epilogue(std::false_type{});
 }
 
-// Decoding step (M <= 16 rows: one row per window).  A workgroup of four
-// waves owns 64 columns; wave w accumulates the 16-column block c + 16 w and
-// runs, for every output element, the same chain as gemm_bf16_kernel:
-// 16x16x32 bf16 MFMAs over the 32-wide k chunks in increasing order, lane l
-// holding row (l & 15) and k values 8*(l >> 4) .. +8 of a chunk.  So a row's
-// outputs equal, bit for bit, what the tiled kernel gives that row in a
-// batch of whole windows.  Operands come straight from global memory (the
-// step streams the weights once, one block per wave for parallelism),
-// kRowsPf chunks ahead.  Blocks 2 and 3 hand their accumulators to blocks 0
-// and 1 through LDS, which run the epilogue on the (col, col + 32) pairs.
+// Decoding step (M <= 16 rows: one row per window).  Every wave accumulates
+// one 16-column block and runs, for every output element, the same chain as
+// gemm_bf16_kernel: 16x16x32 bf16 MFMAs over the 32-wide k chunks in
+// increasing order, lane l holding row (l & 15) and k values 8*(l >> 4) .. +8
+// of a chunk.  So a row's outputs equal, bit for bit, what the tiled kernel
+// gives that row in a batch of whole windows.  Operands come straight from
+// global memory (the step streams the weights once), kRowsPf chunks ahead.
+// The step is bound by how many weight bytes each wave has in flight, so the
+// waves are spread over as many CUs as the epilogue allows.  NWR waves per
+// workgroup:
+//  - 4: 64 columns; waves 2 and 3 hand their accumulators to waves 0 and 1
+//    through LDS, which run the epilogue on the (col, col + 32) pairs (QKV:
+//    the RoPE pairs and the transposed V stores);
+//  - 2: the two blocks c and c + 32 of one pair (gate/up, GELU, float32
+//    store);
+//  - 1: one block, for the residual add, which pairs nothing (N = d = 4096 has
+//    only 256 blocks: one wave on each CU instead of 64 four-wave groups).
 constexpr int kRowsPf = 16;
 
-template <int KIND, int HD>
-__global__ __launch_bounds__(256) void gemm_bf16_rows_kernel(const uint16_t* __restrict__ A,
-                                                             const uint16_t* __restrict__ Bw, int M,
-                                                             int K, EpiArgs e) {
-  __shared__ f32x4 part[2][64];  // accumulators of blocks 2 and 3
+template <int KIND, int HD, int NWR>
+__global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t* __restrict__ A,
+                                                                  const uint16_t* __restrict__ Bw,
+                                                                  int M, int K, EpiArgs e) {
+  __shared__ f32x4 part[NWR == 4 ? 2 : 1][64];  // accumulators handed to the pair's first block
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + wave * 16;  // this wave's block
+  int c;  // this wave's block
+  if (NWR == 4) c = blockIdx.x * 64 + wave * 16;
+  else if (NWR == 2) c = (blockIdx.x >> 1) * 64 + (blockIdx.x & 1) * 16 + wave * 32;
+  else c = blockIdx.x * 16;
   const int r = lane & 15, kq = lane >> 4;
   // rows past M re-read row M - 1; they only feed outputs that are not stored
   const u32x4* pa = reinterpret_cast<const u32x4*>(A + (int64_t)min(r, M - 1) * K + kq * 8);
@@ -388,48 +398,76 @@ __global__ __launch_bounds__(256) void gemm_bf16_rows_kernel(const uint16_t* __r
       mma(0);
     }
   }
-  if (wave >= 2) part[wave - 2][lane] = acc;
-  __syncthreads();
-  if (wave >= 2) return;
-  const f32x4 hi = part[wave][lane];  // block c + 32, same lane layout
-  // lane holds column c + (lane & 15) (paired with + 32) and rows 4 kq + i
+  // lane holds column c + (lane & 15) and rows 4 kq + i
   using E = Epi<uint16_t, KIND, HD>;
   const int col = c + r;
-  const ColInfo ci = E::column(e, col);
+  if constexpr (NWR == 1) {
+    static_assert(KIND == EPI_RESID, "single blocks only for the residual add");
+    if (col >= e.N) return;
+    const float bias = e.bias ? load_par<uint16_t>(e.bias, col) : 0.f;
 #pragma unroll
-  for (int i = 0; i < 4; i++) {
-    const int row = 4 * kq + i;
-    if (row < M) E::row(e, ci, col, row, row, e.dpos, acc[i], hi[i]);
+    for (int i = 0; i < 4; i++) {
+      const int row = 4 * kq + i;
+      if (row < M) {
+        float* p = e.c + (int64_t)row * e.ldc;
+        p[col] = resid_add(p[col], acc[i], bias);
+      }
+    }
+  } else {
+    constexpr int NH = NWR / 2;  // the second half of the waves hand over
+    if (wave >= NH) part[wave - NH][lane] = acc;
+    __syncthreads();
+    if (wave >= NH) return;
+    const f32x4 hi = part[wave][lane];  // block c + 32, same lane layout
+    const ColInfo ci = E::column(e, col);
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int row = 4 * kq + i;
+      if (row < M) E::row(e, ci, col, row, row, e.dpos, acc[i], hi[i]);
+    }
   }
 }
 
+template <int KIND, int HD>
+hipError_t launch_rows_one(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
+                           const EpiArgs& e, hipStream_t s) {
+  if constexpr (KIND == EPI_RESID) {
+    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 1>), dim3(N_pad / 16), dim3(64), 0, s, A, B, M, K, e);
+  } else if constexpr (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS) {
+    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 4>), dim3(N_pad / 64), dim3(256), 0, s, A, B, M, K, e);
+  } else {
+    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 2>), dim3(N_pad / 32), dim3(128), 0, s, A, B, M, K, e);
+  }
+  return hipGetLastError();
+}
+
+// HD != 0: the QKV kinds of a bf16 model with that head dim; HD == 0: the rest.
 template <int HD>
 hipError_t launch_rows_kind(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
                             const EpiArgs& e, hipStream_t s) {
-  const dim3 grid(N_pad / 64), block(256);  // 4 waves x 16 columns
-  switch (e.kind) {
-    case EPI_STORE_F32:
-      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_STORE_F32, HD>), grid, block, 0, s, A, B, M, K, e);
-      break;
-    case EPI_RESID:
-      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_RESID, HD>), grid, block, 0, s, A, B, M, K, e);
-      break;
-    case EPI_QKV_ROPE:
-      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_QKV_ROPE, HD>), grid, block, 0, s, A, B, M, K, e);
-      break;
-    case EPI_QKV_BIAS:
-      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_QKV_BIAS, HD>), grid, block, 0, s, A, B, M, K, e);
-      break;
-    case EPI_SWIGLU:
-      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_SWIGLU, HD>), grid, block, 0, s, A, B, M, K, e);
-      break;
-    case EPI_BIAS_GELU:
-      hipLaunchKernelGGL((gemm_bf16_rows_kernel<EPI_BIAS_GELU, HD>), grid, block, 0, s, A, B, M, K, e);
-      break;
-    default:
-      return hipErrorInvalidValue;
+  if constexpr (HD != 0) {
+    switch (e.kind) {
+      case EPI_QKV_ROPE:
+        return launch_rows_one<EPI_QKV_ROPE, HD>(A, B, M, N_pad, K, e, s);
+      case EPI_QKV_BIAS:
+        return launch_rows_one<EPI_QKV_BIAS, HD>(A, B, M, N_pad, K, e, s);
+      default:
+        return hipErrorInvalidValue;
+    }
+  } else {
+    switch (e.kind) {
+      case EPI_STORE_F32:
+        return launch_rows_one<EPI_STORE_F32, 0>(A, B, M, N_pad, K, e, s);
+      case EPI_RESID:
+        return launch_rows_one<EPI_RESID, 0>(A, B, M, N_pad, K, e, s);
+      case EPI_SWIGLU:
+        return launch_rows_one<EPI_SWIGLU, 0>(A, B, M, N_pad, K, e, s);
+      case EPI_BIAS_GELU:
+        return launch_rows_one<EPI_BIAS_GELU, 0>(A, B, M, N_pad, K, e, s);
+      default:
+        return hipErrorInvalidValue;
+    }
   }
-  return hipGetLastError();
 }
 
 template <int KIND, int HD>
