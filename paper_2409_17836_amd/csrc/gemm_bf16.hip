@@ -36,8 +36,9 @@
 //
 // Workgroup -> tile order: the hardware deals workgroups to the 8 XCDs
 // round-robin; ids are remapped so each XCD walks a contiguous range of a
-// row-grouped tile order (4 row-tiles per group), which keeps the A and B
-// panels the co-resident workgroups of an XCD share in that XCD's L2.
+// row-grouped tile order (4 row tiles per group, 8 when the ring holds B),
+// which keeps the A and B panels the co-resident workgroups of an XCD share
+// in that XCD's L2.
 #include "epilogue.h"
 
 namespace lmgc {
@@ -50,7 +51,9 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int kThreads = 512;
-constexpr int kGroupM = 4;
+// row tiles per group of the tile order: 4 when the ring holds A, 8 when it
+// holds B (measured best at the 7B shape)
+constexpr int kGroupM = 4, kGroupMB = 8;
 constexpr int kXcds = 8;
 constexpr int kLoadEvery = 4;  // MFMAs between two operand loads of a wave
 // s_waitcnt immediates (vmcnt in bits 3:0, expcnt and lgkmcnt left at their maxima)
@@ -60,15 +63,16 @@ __device__ inline int slot(int row, int chunk) { return row * 8 + (chunk ^ ((row
 
 __device__ inline bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+template <int GM>
 __device__ inline bool map_tile(int bid, int nblocks, int ntm, int ntn, int& tm, int& tn) {
   const int total = ntm * ntn;
   const int per = nblocks / kXcds;  // nblocks is a multiple of kXcds
   const int t = (bid % kXcds) * per + bid / kXcds;
   if (t >= total) return false;
-  const int in_group = kGroupM * ntn;
+  const int in_group = GM * ntn;
   const int g = t / in_group;
-  const int first = g * kGroupM;
-  const int gs = min(ntm - first, kGroupM);
+  const int first = g * GM;
+  const int gs = min(ntm - first, GM);
   const int r = t - g * in_group;
   tm = first + r % gs;
   tn = r / gs;
@@ -90,7 +94,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   __shared__ u32x4 sD0[BN * 8], sD1[BN * 8];               // 2 x 32 KB
 
   int tm, tn;
-  if (!map_tile(blockIdx.x, gridDim.x, ntm, ntn, tm, tn)) return;
+  if (!map_tile<RB ? kGroupMB : kGroupM>(blockIdx.x, gridDim.x, ntm, ntn, tm, tn)) return;
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int tid = threadIdx.x;
