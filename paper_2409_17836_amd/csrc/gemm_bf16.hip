@@ -55,7 +55,8 @@ constexpr int kThreads = 512;
 // holds B (measured best at the 7B shape)
 constexpr int kGroupM = 4, kGroupMB = 8;
 constexpr int kXcds = 8;
-constexpr int kLoadEvery = 4;  // MFMAs between two operand loads of a wave
+// MFMAs between two operand loads of a wave (ring on A / ring on B)
+constexpr int kLoadEvery = 4, kLoadEveryB = 3;
 // s_waitcnt immediates (vmcnt in bits 3:0, expcnt and lgkmcnt left at their maxima)
 constexpr int kVmcnt0 = 0xF70, kVmcnt4 = 0xF74;
 
@@ -136,7 +137,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   };
   // One stage from ring buffer sr and double buffer sd.  The double-buffered
   // operand of stage kd goes to nd and the ring operand of stage kr to nr
-  // (negative: no load), one load after every kLoadEvery MFMAs.
+  // (negative: no load), one load after every kLoadEvery (kLoadEveryB) MFMAs.
   auto ld_r = [&](u32x4* buf, int i, int k0) __attribute__((always_inline)) {
     if (RB) ldB(buf, i, k0);
     else ldA(buf, i, k0);
@@ -163,7 +164,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
 #pragma unroll
         for (int j = 0; j < 4; j++) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
-          if (++nm % kLoadEvery == 0 && issued < 8) {
+          if (++nm % (RB ? kLoadEveryB : kLoadEvery) == 0 && issued < 8) {
             __builtin_amdgcn_sched_barrier(0);
             if (issued < 4) {
               if (kd >= 0) ld_d(nd, issued, kd);
