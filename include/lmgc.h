@@ -404,6 +404,13 @@ enum {
 };
 /* Enable (1) or disable (0) timing and clear the accumulated times. */
 int lmgc_timing_enable(int32_t enable);
+/*
+ * Record events only around launches of the kinds in `kind_mask` (bit k =
+ * kind k; the default is every kind).  Each recorded pair adds a little
+ * time between launches, so a timed run can restrict them to the kernel it
+ * reports.  EINVAL if the mask has no valid kind.
+ */
+int lmgc_timing_kinds(uint32_t kind_mask);
 /* Synchronise pending events; total milliseconds and launches of `kind`. */
 int lmgc_timing_read(int32_t kind, double* total_ms, int64_t* count);
 /* Algorithmic floating-point operations of one lmgc_probs call, by kind. */

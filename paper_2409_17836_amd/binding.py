@@ -101,6 +101,7 @@ def lib():
         "lmgc_op_gemm_bf16": (ctypes.c_int, [vp, vp, vp, i32, i32, i32, vp]),
         "lmgc_op_attention_bf16": (ctypes.c_int, [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]),
         "lmgc_timing_enable": (ctypes.c_int, [i32]),
+        "lmgc_timing_kinds": (ctypes.c_int, [u32]),
         "lmgc_timing_read": (ctypes.c_int, [i32, P(ctypes.c_double), P(i64)]),
         "lmgc_probs_flops": (ctypes.c_double, [vp, i32, i32, i32]),
     }
@@ -478,6 +479,15 @@ def op_attention_bf16(q, k, vt, o=None, stream=None):
 # ----------------------------------------------------------------- timing --
 def timing_enable(on: bool = True):
     _check(lib().lmgc_timing_enable(1 if on else 0))
+
+
+def timing_kinds(kinds=None):
+    """lmgc_timing_kinds: record events only for these kinds (None: all)."""
+    names = list(KIND) if kinds is None else list(kinds)
+    mask = 0
+    for k in names:
+        mask |= 1 << KIND[k]
+    _check(lib().lmgc_timing_kinds(mask))
 
 
 def timing_read(kind: str) -> Tuple[float, int]:

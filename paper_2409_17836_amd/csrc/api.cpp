@@ -82,6 +82,7 @@ static int check_serial(const lmgc_serial_params* p, int vocab) {
 struct Timing {
   std::mutex mu;
   bool on = false;
+  uint32_t mask = (1u << LMGC_K_COUNT) - 1;  // kinds whose launches get events
   std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[LMGC_K_COUNT];
   double ms[LMGC_K_COUNT] = {};
   int64_t count[LMGC_K_COUNT] = {};
@@ -95,7 +96,7 @@ struct ScopedTimer {
   hipEvent_t a = nullptr, b = nullptr;
   ScopedTimer(int k, hipStream_t st) : kind(k), s(st) {
     std::lock_guard<std::mutex> g(g_timing.mu);
-    if (!g_timing.on) return;
+    if (!g_timing.on || !((g_timing.mask >> kind) & 1u)) return;
     for (hipEvent_t* e : {&a, &b}) {
       if (!g_timing.pool.empty()) {
         *e = g_timing.pool.back();
@@ -1168,6 +1169,14 @@ int lmgc_timing_enable(int32_t enable) {
     g_timing.ms[k] = 0;
     g_timing.count[k] = 0;
   }
+  return LMGC_OK;
+}
+
+int lmgc_timing_kinds(uint32_t kind_mask) {
+  kind_mask &= (1u << LMGC_K_COUNT) - 1;
+  if (!kind_mask) return set_error(LMGC_EINVAL, "lmgc_timing_kinds: no valid kind in the mask");
+  std::lock_guard<std::mutex> g(g_timing.mu);
+  g_timing.mask = kind_mask;
   return LMGC_OK;
 }
 

@@ -26,6 +26,15 @@ def test_library_exports_every_declared_symbol():
     assert not missing, missing
 
 
+def test_timing_kinds_mask():
+    """lmgc_timing_kinds takes a mask of kernel kinds; an empty one is an error."""
+    B.timing_kinds(["gemm_up"])
+    B.timing_kinds(None)
+    assert B.lib().lmgc_timing_kinds(0) == -1  # LMGC_EINVAL
+    assert B.lib().lmgc_timing_kinds(1 << 31) == -1  # no valid kind
+    assert b"no valid kind" in B.lib().lmgc_last_error()
+
+
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
 def test_manifest_matches_generator(name):
     w = WORKLOADS[name]
