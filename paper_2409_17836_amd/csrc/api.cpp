@@ -230,7 +230,8 @@ static int copy_tensor(lmgc_model* m, const void* src, size_t bytes, hipStream_t
   return LMGC_OK;
 }
 
-// Repack rows: out[r] = srcs[idx[r] >> 28][idx[r] & 0x0fffffff] (or zeros).
+// Repack rows: out[r] = srcs[idx[r] >> 28][idx[r] & 0x0fffffff] (or zeros);
+// bf16 matrices are written in MFMA blocks.
 static int gather_tensor(lmgc_model* m, GatherSrcs srcs, const std::vector<int32_t>& idx, int cols,
                          hipStream_t s, std::vector<void*>& temps, const void** out) {
   const size_t row_bytes = (size_t)cols * m->act;
@@ -241,7 +242,11 @@ static int gather_tensor(lmgc_model* m, GatherSrcs srcs, const std::vector<int32
   HIP_OK(hipMalloc(&d_idx, idx.size() * sizeof(int32_t)));
   temps.push_back(d_idx);
   HIP_OK(hipMemcpyAsync(d_idx, idx.data(), idx.size() * sizeof(int32_t), hipMemcpyHostToDevice, s));
-  HIP_OK(launch_gather_rows(srcs, (const int32_t*)d_idx, (int)idx.size(), cols, m->act, p, s));
+  // bf16 weights go to MFMA blocks (the layout the matrix kernels take B in)
+  if (m->act == 2)
+    HIP_OK(launch_gather_rows_blocked(srcs, (const int32_t*)d_idx, (int)idx.size(), cols, p, s));
+  else
+    HIP_OK(launch_gather_rows(srcs, (const int32_t*)d_idx, (int)idx.size(), cols, m->act, p, s));
   *out = p;
   return LMGC_OK;
 }
@@ -1140,7 +1145,7 @@ int lmgc_op_gemm_bf16(const uint16_t* d_a, const uint16_t* d_b, float* d_c, int3
   e.N = N;
   e.c = d_c;
   e.ldc = N;
-  hipError_t err = launch_gemm_bf16(d_a, d_b, M, N, K, e, (hipStream_t)stream);
+  hipError_t err = launch_gemm_bf16(d_a, d_b, M, N, K, e, (hipStream_t)stream, false);
   if (err != hipSuccess) return set_error(LMGC_EDEVICE, "gemm launch: %s", hipGetErrorString(err));
   return LMGC_OK;
 }

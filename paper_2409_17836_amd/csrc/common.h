@@ -79,12 +79,26 @@ hipError_t launch_embed(const int32_t* tokens, int B, int W, int bos_id, const v
 hipError_t launch_norm(const float* h, int M, int d, const void* gain, const void* bias,
                        int layernorm, float eps, int dtype, void* y, hipStream_t s);
 
+// Weight matrices of bf16 models are stored in MFMA blocks: for B [N, K]
+// (N % 16 == 0, K % 32 == 0), block (n / 16, k / 32) holds 16 rows x 32 k as
+// 1 KB in the order the 64 lanes of a 16x16x32 MFMA take their B operand:
+// element (n, k) sits at block ((n/16) * (K/32) + k/32), lane
+// (n % 16) + 16 * ((k % 32) / 8), position k % 8.  Blocks of one 16-row
+// group are consecutive, so a tile of rows n0 .. n0+255 starts at n0 * K, as
+// in row-major order.
+__host__ __device__ inline int64_t blocked_index(int64_t n, int64_t k, int64_t K) {
+  return ((n >> 4) * (K >> 5) + (k >> 5)) * 512 + ((n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
+}
+
+// blocked_b: B in MFMA blocks (the model's weights) or row-major [N, K] (only
+// for the float32 store, the exposed operator).
 hipError_t launch_gemm_bf16(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
-                            const EpiArgs& e, hipStream_t s);
+                            const EpiArgs& e, hipStream_t s, bool blocked_b = true);
 hipError_t launch_gemm_f32(const float* A, const float* B, int M, int N_pad, int K,
                            const EpiArgs& e, hipStream_t s);
 // Decoding step: M <= 16 rows, each output element accumulated exactly as
-// launch_gemm_bf16 accumulates it (same MFMA, operand layout and k order).
+// launch_gemm_bf16 accumulates it (same MFMA, operand layout and k order);
+// B in MFMA blocks.
 hipError_t launch_gemm_bf16_rows(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
                                  const EpiArgs& e, hipStream_t s);
 
@@ -105,6 +119,7 @@ hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int3
 
 // dst [rows, cols]: row r < n_alpha = head row alpha_ids[r] (host array),
 // the remaining rows zero.  Rows are cols * elem_bytes bytes (multiple of 4).
+// elem_bytes == 2: head and dst are in MFMA blocks (rows % 16 == 0).
 hipError_t launch_alpha_head(const void* head, const int32_t* alpha_ids, int n_alpha, int rows, int cols,
                              int elem_bytes, void* dst, hipStream_t s);
 
@@ -131,5 +146,9 @@ struct GatherSrcs {
 };
 hipError_t launch_gather_rows(GatherSrcs srcs, const int32_t* idx, int rows, int cols,
                               int elem_bytes, void* dst, hipStream_t s);
+// The same gather of bf16 rows, written in MFMA blocks (rows % 16 == 0,
+// cols % 32 == 0).
+hipError_t launch_gather_rows_blocked(GatherSrcs srcs, const int32_t* idx, int rows, int cols,
+                                      void* dst, hipStream_t s);
 
 }  // namespace lmgc

@@ -241,6 +241,22 @@ __global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int 
 
 // Rows of the LM head for the alphabet tokens: dst row r (r < na) = head row
 // ids[r]; rows na..gridDim.x-1 are zero.  One block per row.
+// bf16: head and tile in MFMA blocks; one thread per 16-byte piece (8
+// values of one row) of the tile.
+__global__ void alpha_head_blocked_kernel(const uint4* __restrict__ head, AlphaIds ids, int na, int rows,
+                                          int cols, uint4* __restrict__ dst) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int pieces = cols / 8;
+  if (t >= (int64_t)rows * pieces) return;
+  const int r = (int)(t / pieces), q = (int)(t - (int64_t)r * pieces);
+  const int64_t di = blocked_index(r, 8 * q, cols) / 8;
+  if (r >= na) {
+    dst[di] = make_uint4(0u, 0u, 0u, 0u);
+    return;
+  }
+  dst[di] = head[blocked_index(ids.v[r], 8 * q, cols) / 8];
+}
+
 __global__ void alpha_head_kernel(const uint32_t* __restrict__ head, AlphaIds ids, int na, int words,
                                   uint32_t* __restrict__ dst) {
   const int r = blockIdx.x;
@@ -254,6 +270,23 @@ __global__ void alpha_head_kernel(const uint32_t* __restrict__ head, AlphaIds id
 }
 
 // ------------------------------------------------------------------ gather
+// bf16 rows into MFMA blocks: one thread per 16-byte piece of an output row.
+__global__ void gather_rows_blocked_kernel(GatherSrcs srcs, const int32_t* __restrict__ idx, int rows,
+                                           int cols, uint4* __restrict__ dst) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int pieces = cols / 8;
+  if (t >= (int64_t)rows * pieces) return;
+  const int r = (int)(t / pieces), q = (int)(t - (int64_t)r * pieces);
+  const int64_t di = blocked_index(r, 8 * q, cols) / 8;
+  const int32_t id = idx[r];
+  if (id < 0) {
+    dst[di] = make_uint4(0u, 0u, 0u, 0u);
+    return;
+  }
+  const uint4* src = (const uint4*)srcs.p[id >> 28] + (int64_t)(id & 0x0fffffff) * pieces;
+  dst[di] = src[q];
+}
+
 __global__ void gather_rows_kernel(GatherSrcs srcs, const int32_t* __restrict__ idx, int rows,
                                    int words, uint32_t* __restrict__ dst) {
   const int r = blockIdx.x;
@@ -341,8 +374,24 @@ hipError_t launch_alpha_head(const void* head, const int32_t* alpha_ids, int n_a
   if (n_alpha < 1 || n_alpha > LMGC_NALPHA_MAX || rows < n_alpha || (cols * elem_bytes) % 4)
     return hipErrorInvalidValue;
   for (int a = 0; a < n_alpha; a++) ids.v[a] = alpha_ids[a];
+  if (elem_bytes == 2) {
+    if (rows % 16 || cols % 32) return hipErrorInvalidValue;
+    const int64_t n = (int64_t)rows * (cols / 8);
+    hipLaunchKernelGGL(alpha_head_blocked_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       (const uint4*)head, ids, n_alpha, rows, cols, (uint4*)dst);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(alpha_head_kernel, dim3((unsigned)rows), dim3(256), 0, s, (const uint32_t*)head, ids, n_alpha,
                      cols * elem_bytes / 4, (uint32_t*)dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows_blocked(GatherSrcs srcs, const int32_t* idx, int rows, int cols,
+                                      void* dst, hipStream_t s) {
+  if (rows % 16 || cols % 32) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)rows * (cols / 8);
+  hipLaunchKernelGGL(gather_rows_blocked_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, srcs, idx,
+                     rows, cols, (uint4*)dst);
   return hipGetLastError();
 }
 

@@ -86,7 +86,7 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
 }
 
-template <int KIND, int HD, bool RB>
+template <int KIND, int HD, bool RB, bool BLKB>
 __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ Bw, int M, int K, int ntm,
     int ntn, EpiArgs e) {
@@ -116,6 +116,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     const int lc = (lane & 7) ^ ((row >> 1) & 7);
     voff[i] = (row * K + lc * 8) * 2;
   }
+  // BLKB: B in MFMA blocks.  A stage's B tile is 32 blocks of 1 KB (16 row
+  // groups x two 32-wide k chunks); load i of wave w copies block w*4 + i =
+  // 16 kc + j (row group j, chunk kc of the stage) to the same place in LDS,
+  // where lane l's 16 bytes are already its MFMA operand: no swizzle.
+  int voffb[4];
+#pragma unroll
+  for (int i = 0; i < 4; i++) {
+    const int blk = wave * 4 + i, kc = blk >> 4, j = blk & 15;
+    voffb[i] = BLKB ? ((j * (K / 32) + kc) * 1024 + lane * 16) : voff[i];
+  }
 
   f32x4 acc[8][4];
 #pragma unroll
@@ -132,8 +142,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
                                              k0 * 2, 0, 0);
   };
   auto ldB = [&](u32x4* sb, int i, int k0) __attribute__((always_inline)) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(sb + (wave * 4 + i) * 64), 16, voff[i],
-                                             k0 * 2, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(sb + (wave * 4 + i) * 64), 16, voffb[i],
+                                             BLKB ? k0 * 32 : k0 * 2, 0, 0);
   };
   // One stage from ring buffer sr and double buffer sd.  The double-buffered
   // operand of stage kd goes to nd and the ring operand of stage kr to nr
@@ -158,7 +168,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
 #pragma unroll
       for (int i = 0; i < 8; i++) af[i] = as_bf16x8(sa[slot(arow0 + 16 * i, ch)]);
 #pragma unroll
-      for (int j = 0; j < 4; j++) bf[j] = as_bf16x8(sb[slot(brow0 + 16 * j, ch)]);
+      for (int j = 0; j < 4; j++)
+        bf[j] = as_bf16x8(BLKB ? sb[(ks * 16 + wn * 4 + j) * 64 + lane] : sb[slot(brow0 + 16 * j, ch)]);
 #pragma unroll
       for (int i = 0; i < 8; i++)
 #pragma unroll
@@ -363,13 +374,15 @@ __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t
   const int r = lane & 15, kq = lane >> 4;
   // rows past M re-read row M - 1; they only feed outputs that are not stored
   const u32x4* pa = reinterpret_cast<const u32x4*>(A + (int64_t)min(r, M - 1) * K + kq * 8);
-  const u32x4* pb = reinterpret_cast<const u32x4*>(Bw + (int64_t)(c + r) * K + kq * 8);
+  // B in MFMA blocks: the wave's 16 rows are one contiguous stream of 1 KB
+  // blocks, lane l's 16 bytes at 16 l of each
+  const int nkc = K / 32;  // A chunk kc starts at u32x4 index 4 * kc
+  const u32x4* pb = reinterpret_cast<const u32x4*>(Bw) + (int64_t)(c / 16) * nkc * 64 + lane;
   f32x4 acc = f32x4{};
-  const int nkc = K / 32;  // chunk kc starts at u32x4 index 4 * kc
   u32x4 fa[kRowsPf], fb[kRowsPf];
   auto fetch = [&](int u, int kc) __attribute__((always_inline)) {
     fa[u] = pa[4 * kc];
-    fb[u] = pb[4 * kc];
+    fb[u] = pb[(int64_t)kc * 64];
   };
   auto mma = [&](int u) __attribute__((always_inline)) {
     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[u]), as_bf16x8(fb[u]), acc, 0, 0, 0);
@@ -475,47 +488,53 @@ hipError_t launch_rows_kind(const uint16_t* A, const uint16_t* B, int M, int N_p
   }
 }
 
-template <int KIND, int HD>
+template <int KIND, int HD, bool BLKB>
 hipError_t launch_one(const uint16_t* A, const uint16_t* B, int M, int K, int ntm, int ntn, bool rb,
                       const EpiArgs& e, hipStream_t s) {
   const int total = ntm * ntn;
   const dim3 grid((total + kXcds - 1) / kXcds * kXcds), block(kThreads);
   if constexpr (KIND == EPI_RESID) {
     (void)rb;  // the residual products (N = d) keep the ring on A
-    hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, false>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
+    hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, false, BLKB>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
   } else {
     if (rb)
-      hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, true>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
+      hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, true, BLKB>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
     else
-      hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, false>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
+      hipLaunchKernelGGL((gemm_bf16_kernel<KIND, HD, false, BLKB>), grid, block, 0, s, A, B, M, K, ntm, ntn, e);
   }
   return hipGetLastError();
 }
 
 // HD != 0: the QKV kinds of a bf16 model with that head dim; HD == 0: the rest.
+// Row-major B (blocked == false) only for the float32 store.
 template <int HD>
 hipError_t launch_kind(const uint16_t* A, const uint16_t* B, int M, int K, int ntm, int ntn,
-                       const EpiArgs& e, hipStream_t s) {
+                       const EpiArgs& e, hipStream_t s, bool blocked) {
   const bool rb = (int64_t)ntn * BN >= 2 * (int64_t)K;  // wide weight matrix: the ring holds B
   if constexpr (HD != 0) {
+    if (!blocked) return hipErrorInvalidValue;
     switch (e.kind) {
       case EPI_QKV_ROPE:
-        return launch_one<EPI_QKV_ROPE, HD>(A, B, M, K, ntm, ntn, rb, e, s);
+        return launch_one<EPI_QKV_ROPE, HD, true>(A, B, M, K, ntm, ntn, rb, e, s);
       case EPI_QKV_BIAS:
-        return launch_one<EPI_QKV_BIAS, HD>(A, B, M, K, ntm, ntn, rb, e, s);
+        return launch_one<EPI_QKV_BIAS, HD, true>(A, B, M, K, ntm, ntn, rb, e, s);
       default:
         return hipErrorInvalidValue;
     }
   } else {
+    if (!blocked) {
+      if (e.kind != EPI_STORE_F32) return hipErrorInvalidValue;
+      return launch_one<EPI_STORE_F32, 0, false>(A, B, M, K, ntm, ntn, rb, e, s);
+    }
     switch (e.kind) {
       case EPI_STORE_F32:
-        return launch_one<EPI_STORE_F32, 0>(A, B, M, K, ntm, ntn, rb, e, s);
+        return launch_one<EPI_STORE_F32, 0, true>(A, B, M, K, ntm, ntn, rb, e, s);
       case EPI_RESID:
-        return launch_one<EPI_RESID, 0>(A, B, M, K, ntm, ntn, rb, e, s);
+        return launch_one<EPI_RESID, 0, true>(A, B, M, K, ntm, ntn, rb, e, s);
       case EPI_SWIGLU:
-        return launch_one<EPI_SWIGLU, 0>(A, B, M, K, ntm, ntn, rb, e, s);
+        return launch_one<EPI_SWIGLU, 0, true>(A, B, M, K, ntm, ntn, rb, e, s);
       case EPI_BIAS_GELU:
-        return launch_one<EPI_BIAS_GELU, 0>(A, B, M, K, ntm, ntn, rb, e, s);
+        return launch_one<EPI_BIAS_GELU, 0, true>(A, B, M, K, ntm, ntn, rb, e, s);
       default:
         return hipErrorInvalidValue;
     }
@@ -536,15 +555,15 @@ hipError_t launch_gemm_bf16_rows(const uint16_t* A, const uint16_t* B, int M, in
 }
 
 hipError_t launch_gemm_bf16(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
-                            const EpiArgs& e, hipStream_t s) {
+                            const EpiArgs& e, hipStream_t s, bool blocked_b) {
   if (M <= 0) return hipSuccess;
   if (e.step || K % BK != 0 || N_pad % BN != 0) return hipErrorInvalidValue;
   const int ntm = (M + BM - 1) / BM, ntn = N_pad / BN;
   const bool qkv = e.kind == EPI_QKV_ROPE || e.kind == EPI_QKV_BIAS;
-  if (qkv && e.hd == 128) return launch_kind<128>(A, B, M, K, ntm, ntn, e, s);
-  if (qkv && e.hd == 64) return launch_kind<64>(A, B, M, K, ntm, ntn, e, s);
+  if (qkv && e.hd == 128) return launch_kind<128>(A, B, M, K, ntm, ntn, e, s, blocked_b);
+  if (qkv && e.hd == 64) return launch_kind<64>(A, B, M, K, ntm, ntn, e, s, blocked_b);
   if (qkv) return hipErrorInvalidValue;
-  return launch_kind<0>(A, B, M, K, ntm, ntn, e, s);
+  return launch_kind<0>(A, B, M, K, ntm, ntn, e, s, blocked_b);
 }
 
 }  // namespace lmgc
