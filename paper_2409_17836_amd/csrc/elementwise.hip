@@ -185,6 +185,10 @@ __global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int 
   const float* zr = z + row * (int64_t)ldz;
   float m = -INFINITY, s = 0.f;
   const int V4 = V & ~3;
+  // (unrolled so that several loads are in flight: a few rows, as in a
+  // decoding step, are bound by load latency; the per-lane order of the
+  // arithmetic is unchanged)
+#pragma unroll 8
   for (int c = lane * 4; c < V4; c += kWave * 4) {
     const float4 t = *reinterpret_cast<const float4*>(zr + c);
     const float mx = fmaxf(fmaxf(t.x, t.y), fmaxf(t.z, t.w));
