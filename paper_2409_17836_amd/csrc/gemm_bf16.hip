@@ -1,7 +1,9 @@
 // bf16 matrix product on CDNA4 matrix cores: C[M, N] = A[M, K] * B[N, K]^T
 // with float32 accumulation, followed by a fused epilogue (epilogue.h).
 //
-// Both operands are K-contiguous (activations row-major, weights [out, in]).
+// Both operands are K-contiguous: activations row-major, weights [out, in]
+// in MFMA blocks (BLKB; common.h: 16 rows x 32 k per 1 KB in the order the
+// lanes take their operand) or row-major (the exposed float32-store product).
 // Tile: 256 x 256 output per 512-thread workgroup: eight 64-wide waves, two
 // per SIMD so that one wave's LDS reads and waits overlap the other's matrix
 // instructions; wave (wm, wn) owns rows wm*128 .. +128 and columns
@@ -16,18 +18,21 @@
 // gate/up, QKV, LM head) has new B panels for every wave of tiles, while an
 // XCD's A panels repeat; for a narrow one (the N = d products that add into
 // the residual) B stays cached and A streams.  A wave's eight loads of a
-// stage are spread through its MFMA stream (one after every four MFMAs)
-// instead of being issued in one burst after the barrier: all workgroups
+// stage are spread through its MFMA stream (one after every four MFMAs, three
+// when the ring holds B) instead of being issued in one burst after the
+// barrier: all workgroups
 // bursting at once queue in L2 and roughly double the load latency.  Each
 // buffer is its own __shared__ array, so the compiler can tell the in-flight
 // loads of one buffer from the reads of another.  The buffer resources are
 // per tile with the tile's valid rows as their size: rows past M read as
 // zero (and only feed outputs that are never stored).
 //
-// A 256 x 64 operand tile is stored as rows of eight 16-byte chunks; chunk c
-// of row r sits at slot c ^ ((r >> 1) & 7): the 16 lanes that one
-// ds_read_b128 cycle serves read 16 consecutive rows, and the swizzle gives
-// every (row parity, slot) pair once, i.e. all 64 banks.
+// A row-major 256 x 64 operand tile is stored as rows of eight 16-byte
+// chunks; chunk c of row r sits at slot c ^ ((r >> 1) & 7): the 16 lanes that
+// one ds_read_b128 cycle serves read 16 consecutive rows, and the swizzle
+// gives every (row parity, slot) pair once, i.e. all 64 banks.  A blocked B
+// tile is its 32 blocks copied as they are: lane l reads 16 bytes at 16 l of
+// a block, conflict-free without a swizzle.
 //
 // Determinism: every output element is the same fixed sequence of MFMA
 // accumulations over k regardless of M, of the tile it sits in, and of the
