@@ -26,6 +26,91 @@ def test_library_exports_every_declared_symbol():
     assert not missing, missing
 
 
+_C_SCALARS = {  # C type -> (size, signed, is_float)
+    "int": (4, True, False), "int32_t": (4, True, False), "int64_t": (8, True, False),
+    "uint32_t": (4, False, False), "uint64_t": (8, False, False), "size_t": (8, False, False),
+    "float": (4, True, True), "double": (8, True, True), "uint8_t": (1, False, False),
+    "uint16_t": (2, False, False), "char": (1, True, False), "void": (0, False, False),
+}
+_C_STRUCTS = {"lmgc_serial_params": "SerialParams", "lmgc_model_config": "ModelConfig",
+              "lmgc_decoder": "DecoderState"}
+
+
+def _prototypes(text):
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    text = re.sub(r"(?m)^\s*#.*$", " ", text)
+    out = {}
+    for m in re.finditer(r"([A-Za-z_][\w \t\*]*?)\b(lmgc_[a-z0-9_]+)\s*\(([^;{]*?)\)\s*;", text):
+        ret, name, args = m.group(1), m.group(2), m.group(3).strip()
+        params = [] if args in ("", "void") else [a.strip() for a in args.split(",")]
+        out[name] = (ret.strip(), params)
+    return out
+
+
+def _ctype_of(decl):
+    """(pointer depth, base type name) of a C parameter or return type."""
+    decl = decl.replace("const", " ")
+    depth = decl.count("*")
+    words = decl.replace("*", " ").split()
+    base = words[0]
+    return depth, base
+
+
+def _check_type(decl, ct, where):
+    import ctypes
+    depth, base = _ctype_of(decl)
+    if depth == 0:
+        size, signed, is_float = _C_SCALARS[base]
+        if base == "void":
+            assert ct is None, where
+            return
+        assert ct is not None and ctypes.sizeof(ct) == size, (where, decl, ct)
+        if is_float:
+            assert ct in (ctypes.c_float, ctypes.c_double), (where, decl, ct)
+        else:
+            assert ct not in (ctypes.c_float, ctypes.c_double), (where, decl, ct)
+            signed_types = (ctypes.c_byte, ctypes.c_short, ctypes.c_int, ctypes.c_long,
+                            ctypes.c_longlong)
+            assert (ct in signed_types) == signed, (where, decl, ct)
+        return
+    # pointers: void* / char* / POINTER(T) with T matching the pointee
+    if ct in (ctypes.c_void_p, ctypes.c_char_p):
+        assert ct is ctypes.c_void_p or (base == "char" and depth == 1), (where, decl, ct)
+        return
+    assert hasattr(ct, "_type_") and issubclass(ct, ctypes._Pointer), (where, decl, ct)
+    inner = ct._type_
+    if depth == 1 and base in _C_STRUCTS:
+        assert inner.__name__ == _C_STRUCTS[base], (where, decl, ct)
+    elif depth == 1:
+        _check_type(base, inner, where)
+    else:  # T** (or T* const*): a pointer to pointers
+        assert inner is ctypes.c_void_p, (where, decl, ct)
+
+
+def test_binding_signatures_match_header():
+    """Every entry point of include/lmgc.h is bound with the declared number of
+    arguments, and each argument and result has the declared size, signedness
+    and pointer-ness (a mismatch would pass garbage without any error)."""
+    protos = _prototypes(open(HEADER).read())
+    assert len(protos) >= 30
+    L = B.lib()
+    for name, (ret, params) in protos.items():
+        f = getattr(L, name)
+        assert f.argtypes is not None, name
+        assert len(f.argtypes) == len(params), (name, params, f.argtypes)
+        for i, (p, ct) in enumerate(zip(params, f.argtypes)):
+            # drop the parameter name (the last word unless the type ends in '*');
+            # an array parameter ("int64_t shape[2]") is a pointer
+            if "[" in p:
+                p = p[:p.index("[")].rsplit(None, 1)[0] + "*"
+            decl = p if p.rstrip().endswith("*") else p.rsplit(None, 1)[0]
+            if "*" in p and not decl.endswith("*"):
+                decl = p[:p.rfind("*") + 1]
+            _check_type(decl, ct, f"{name} arg {i}")
+        _check_type(ret, f.restype, f"{name} result")
+
+
 def test_timing_kinds_mask():
     """lmgc_timing_kinds takes a mask of kernel kinds; an empty one is an error."""
     B.timing_kinds(["gemm_up"])
