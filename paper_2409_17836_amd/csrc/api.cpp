@@ -816,7 +816,7 @@ static int compress(const lmgc_model* m, const void* d_values, int64_t n_values,
   h.total = total;
   h.n_windows = n_windows;
   write_header(out, h);
-  memcpy(out + LMGC_HEADER_BYTES, bits.data(), 4 * (size_t)n_windows);
+  if (n_windows) memcpy(out + LMGC_HEADER_BYTES, bits.data(), 4 * (size_t)n_windows);
   *used = pos;
   return LMGC_OK;
 }
@@ -836,7 +836,7 @@ static int decode(const lmgc_model* m, const uint8_t* buf, size_t bytes, int32_t
   StepWs sw = carve_step(m, G, W, (char*)ws);
   if (ws_bytes < sw.bytes) return set_error(LMGC_ESIZE, "codec workspace too small: %zu < %zu", ws_bytes, sw.bytes);
   std::vector<uint32_t> bits(h.n_windows);
-  memcpy(bits.data(), buf + LMGC_HEADER_BYTES, 4 * (size_t)h.n_windows);
+  if (h.n_windows) memcpy(bits.data(), buf + LMGC_HEADER_BYTES, 4 * (size_t)h.n_windows);
   std::vector<size_t> off(h.n_windows + 1);
   off[0] = LMGC_HEADER_BYTES + 4 * (size_t)h.n_windows;
   for (int64_t w = 0; w < h.n_windows; w++) off[w + 1] = off[w] + (bits[w] + 7) / 8;

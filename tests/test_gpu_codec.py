@@ -41,6 +41,69 @@ def test_tiny_whole_workload_roundtrip():
     model.close()
 
 
+def test_tiny_empty_and_single_value():
+    """Degenerate inputs: no values give a header-only container (no window,
+    no model call) and one value gives one ragged window of 9 tokens. Both
+    decode back; the headers equal the oracle's byte for byte and the sizes
+    match it (one byte of slack for the float32 against float64 tables)."""
+    import torch
+    w = get_workload("tiny")
+    model, host = build_model(w.model, w.weight_seed)
+    om = OModel(w.model, host)
+    spec = hex_serial(window=256, bos_id=1)
+    sp = B.serial_params(spec)
+    for n in (0, 1):
+        vals = gen_values("laplace:1e-3", n, 3) if n else np.zeros(0, np.float32)
+        log(f"{n} values")
+        buf = B.compress(model, torch.from_numpy(vals).cuda(), sp, batch=4, model_tag=5)
+        ref = opipe.compress(vals, spec, om, model_tag=5)
+        assert buf[:B.HEADER_BYTES] == ref[:B.HEADER_BYTES]
+        assert abs(len(buf) - len(ref)) <= (0 if n == 0 else 1), (len(buf), len(ref))
+        assert B.container_info(buf)["n_windows"] == n
+        back = B.decode(model, buf, batch=4, model_tag=5)
+        assert back.size == n and back.tobytes() == vals.tobytes()
+    model.close()
+
+
+def _split_container(buf, n_windows):
+    """(bit counts, payloads) of a container body holding n_windows windows."""
+    bits = [int(b) for b in np.frombuffer(buf, np.uint32, n_windows, B.HEADER_BYTES)]
+    off = B.HEADER_BYTES + 4 * n_windows
+    pays = []
+    for b in bits:
+        pays.append(buf[off:off + (b + 7) // 8])
+        off += (b + 7) // 8
+    assert off == len(buf)
+    return bits, pays
+
+
+def test_window_ranges_code_like_the_whole_vector():
+    """Coding a range of windows (the benchmark codes one batch of windows per
+    step) gives each window the bits and payload it gets when the whole
+    vector is coded, with another batch size; a range is not a whole-vector
+    container, so decoding rejects it, and a range past the end is an error."""
+    import torch
+    w = get_workload("tiny")
+    model, _ = build_model(w.model, w.weight_seed, keep_host=False)
+    sp = B.serial_params(hex_serial(window=256, bos_id=1))
+    vals = gen_values("laplace:1e-3", 200, 21)  # 1800 tokens: 7 full windows + 8 tokens
+    dv = torch.from_numpy(vals).cuda()
+    full = B.compress(model, dv, sp, batch=3, model_tag=5)
+    nw = B.container_info(full)["n_windows"]
+    assert nw == 8
+    fbits, fpays = _split_container(full, nw)
+    for a, n in [(0, 1), (1, 2), (3, nw - 3), (nw - 1, 1)]:
+        log(f"windows [{a}, {a + n})")
+        part = B.compress(model, dv, sp, batch=2, model_tag=5, first_window=a, n_windows=n)
+        pbits, ppays = _split_container(part, n)
+        assert pbits == fbits[a:a + n] and ppays == fpays[a:a + n]
+        with pytest.raises(B.LMGCError):
+            B.decode(model, part, batch=2, model_tag=5)
+    with pytest.raises(B.LMGCError):
+        B.compress(model, dv, sp, batch=2, first_window=nw - 1, n_windows=2)
+    model.close()
+
+
 def test_tiny_bytes_per_group_variants():
     w = get_workload("tiny")
     model, host = build_model(w.model, w.weight_seed)
