@@ -99,7 +99,12 @@ typedef struct {
 /* Alphabet size A (17 or 18) of these parameters, or < 0 if invalid. */
 int32_t lmgc_alphabet_size(const lmgc_serial_params* p);
 
-/* Tokens in the serialised stream of n_values values (>= 0), or < 0 on error. */
+/* Largest vector the library takes (values): token counts stay far from
+ * int64 overflow.  Larger counts are errors (EINVAL; ECORRUPT in a header). */
+#define LMGC_MAX_VALUES (1LL << 56)
+
+/* Tokens in the serialised stream of n_values values (0 <= n_values <=
+ * LMGC_MAX_VALUES), or < 0 on error. */
 int64_t lmgc_num_tokens(int64_t n_values, const lmgc_serial_params* p);
 /* Windows the stream is cut into (ceil(tokens / W)), or < 0 on error. */
 int64_t lmgc_num_windows(int64_t n_values, const lmgc_serial_params* p);

@@ -737,7 +737,8 @@ static int compress(const lmgc_model* m, const void* d_values, int64_t n_values,
   int rc = check_serial(p, m->cfg.vocab);
   if (rc) return rc;
   if (!d_values && n_values > 0) return set_error(LMGC_EINVAL, "values are NULL");
-  if (!out || !used || n_values < 0 || B <= 0) return set_error(LMGC_EINVAL, "bad arguments");
+  if (!out || !used || n_values < 0 || n_values > LMGC_MAX_VALUES || B <= 0)
+    return set_error(LMGC_EINVAL, "bad arguments");
   const int W = p->window;
   const int64_t nt = num_tokens(n_values, *p);
   const int64_t nw_all = (nt + W - 1) / W;
@@ -919,7 +920,8 @@ int lmgc_serialize(const void* d_values, int64_t n_values, const lmgc_serial_par
   if (((uintptr_t)d_tokens & 15) || ((uintptr_t)d_sym & 3))
     return set_error(LMGC_EINVAL, "d_tokens must be 16-byte and d_sym 4-byte aligned");
   const int64_t nw = lmgc_num_windows(n_values, p);
-  if (first_window < 0 || n_windows < 0 || first_window + n_windows > std::max<int64_t>(nw, 0))
+  if (nw < 0) return set_error(LMGC_EINVAL, "n_values above LMGC_MAX_VALUES");
+  if (first_window < 0 || n_windows < 0 || first_window + n_windows > nw)
     return set_error(LMGC_EINVAL, "window range outside the stream");
   hipError_t e = launch_serialize(d_values, n_values, *p, first_window, n_windows, d_tokens, d_sym,
                                   (hipStream_t)stream);

@@ -244,6 +244,7 @@ int decoder_symbol(lmgc_decoder* st, const uint32_t* c, int nsym, int32_t* out) 
 
 // ---------------------------------------------------------- serialisation
 int64_t num_tokens(int64_t n_values, const lmgc_serial_params& p) {
+  if (n_values < 0 || n_values > LMGC_MAX_VALUES) return -1;
   const int64_t nbytes = n_values * p.bytes_per_value;
   const int64_t groups = p.bytes_per_group > 0 ? (nbytes + p.bytes_per_group - 1) / p.bytes_per_group : 0;
   return 2 * nbytes + groups * (p.sep2_id >= 0 ? 2 : 1);
@@ -320,12 +321,12 @@ int read_header(const uint8_t* buf, size_t bytes, ContainerHeader* c) {
   c->p.pad_id = (int32_t)get_u32(buf + 44);
   c->p.sep_id = (int32_t)get_u32(buf + 48);
   for (int i = 0; i < 16; i++) c->p.hex_ids[i] = (int32_t)get_u32(buf + 52 + 4 * i);
-  c->p.sep2_id = (int32_t)get_u32(buf + 116) - 1;
+  c->p.sep2_id = (int32_t)(get_u32(buf + 116) - 1u);  // 0 (none) -> -1
   c->p.renorm = (int32_t)get_u32(buf + 120);
   if (c->p.renorm != 0 && c->p.renorm != 1) return set_error(LMGC_ECORRUPT, "container: bad table mode");
   if (buf[27] != (c->p.sep2_id >= 0 ? LMGC_NALPHA_MAX + 1 : LMGC_NALPHA + 1))
     return set_error(LMGC_ECORRUPT, "container: symbol count does not match the separators");
-  if (c->n_values < 0 || c->p.window <= 0 ||
+  if (c->n_values < 0 || c->n_values > LMGC_MAX_VALUES || c->p.window <= 0 ||
       (c->p.bytes_per_value != 1 && c->p.bytes_per_value != 2 && c->p.bytes_per_value != 4))
     return set_error(LMGC_ECORRUPT, "container: bad header fields");
   const int64_t nt = num_tokens(c->n_values, c->p);

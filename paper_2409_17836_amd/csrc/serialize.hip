@@ -109,6 +109,7 @@ hipError_t launch_serialize(const void* values, int64_t n_values, const lmgc_ser
   const int threads = 256;
   const int64_t nthreads = (n_local + 3) / 4;
   const int64_t blocks = (nthreads + threads - 1) / threads;
+  if (blocks > INT32_MAX) return hipErrorInvalidValue;
   hipLaunchKernelGGL(serialize_kernel, dim3((unsigned)blocks), dim3(threads), 0, s,
                      (const uint8_t*)values, p, t0, n_local, tokens, sym);
   return hipGetLastError();

@@ -276,3 +276,30 @@ def test_container_info_and_corruption():
         B.container_info(b"XXXX" + buf[4:])
     with pytest.raises(B.LMGCError):
         B.container_info(buf[:100])
+
+
+def test_size_limits_and_hostile_headers():
+    """Vector sizes above LMGC_MAX_VALUES (2^56) are errors rather than int64
+    overflow, and header fields that would overflow (a huge value count, a
+    second-separator field of 2^31) are rejected as corrupt."""
+    import struct
+    sp = B.serial_params(hex_serial(window=4096, bos_id=1))
+    L = B.lib()
+    assert L.lmgc_num_tokens(1 << 56, sp) == 9 * (1 << 56)  # 8 digits + 1 separator
+    assert L.lmgc_num_tokens((1 << 56) + 1, sp) < 0
+    assert L.lmgc_num_tokens(-1, sp) < 0
+    assert L.lmgc_num_windows((1 << 62), sp) < 0
+    ser = hex_serial(window=8, bos_id=1)
+    buf = bytearray(opipe.pack_container(ser, 2, 99, 1 << 16, [13, 20, 5],
+                                         [b"\x01\x02", b"\x03\x04\x05", b"\x06"]))
+    for off, val in [(16, 1 << 62), (16, (1 << 56) + 1), (16, (1 << 64) - 1)]:
+        bad = bytearray(buf)
+        struct.pack_into("<Q", bad, off, val)
+        with pytest.raises(B.LMGCError) as e:
+            B.container_info(bytes(bad))
+        assert e.value.code == -5
+    bad = bytearray(buf)
+    struct.pack_into("<I", bad, 116, 1 << 31)  # sep2_id + 1 = 2^31
+    with pytest.raises(B.LMGCError) as e:
+        B.container_info(bytes(bad))
+    assert e.value.code == -5
