@@ -12,7 +12,8 @@
  * Conventions
  *   - Every call returns an int status (LMGC_OK or a negative LMGC_E* code)
  *     unless stated otherwise; lmgc_last_error() gives a thread-local message.
- *     No C++ exception or abort crosses this ABI.
+ *     No C++ exception or abort crosses this ABI: a failed host allocation
+ *     returns LMGC_ENOMEM.
  *   - The caller owns every buffer.  "d_" pointers are device (HBM) pointers,
  *     "h_"/plain pointers are host pointers.  Size helpers say how much to
  *     allocate.

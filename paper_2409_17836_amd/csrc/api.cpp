@@ -9,7 +9,9 @@
 #include <string.h>
 
 #include <algorithm>
+#include <exception>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -883,6 +885,20 @@ static int decode(const lmgc_model* m, const uint8_t* buf, size_t bytes, int32_t
   return deserialize_bins(sym.data(), nt, h.n_values, h.p, (uint8_t*)values_out);
 }
 
+// Host allocations (std containers, threads) can throw; the ABI reports
+// LMGC_ENOMEM (or LMGC_EDEVICE for any other host exception) instead of
+// letting an exception cross it.
+template <class F>
+static auto guarded(F&& f) -> decltype(f()) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    return (decltype(f()))set_error(LMGC_ENOMEM, "host memory allocation failed");
+  } catch (const std::exception& e) {
+    return (decltype(f()))set_error(LMGC_EDEVICE, "host error: %s", e.what());
+  }
+}
+
 }  // namespace lmgc
 
 // ===================================================================== ABI
@@ -1017,7 +1033,7 @@ int lmgc_sign_pack(const float* d_values, int64_t n_values, uint8_t* d_out, void
 int32_t lmgc_model_num_tensors(const lmgc_model_config* cfg) {
   clear_error();
   if (check_config(cfg)) return -1;
-  return (int32_t)manifest(*cfg).size();
+  return guarded([&] { return (int32_t)manifest(*cfg).size(); });
 }
 
 int lmgc_model_tensor_info(const lmgc_model_config* cfg, int32_t index, char* name, size_t name_cap,
@@ -1025,7 +1041,8 @@ int lmgc_model_tensor_info(const lmgc_model_config* cfg, int32_t index, char* na
   clear_error();
   int rc = check_config(cfg);
   if (rc) return rc;
-  const auto man = manifest(*cfg);
+  std::vector<TensorInfo> man;
+  if ((rc = guarded([&] { man = manifest(*cfg); return LMGC_OK; }))) return rc;
   if (index < 0 || (size_t)index >= man.size()) return set_error(LMGC_EINVAL, "tensor index out of range");
   const TensorInfo& t = man[index];
   if (name && name_cap) {
@@ -1042,7 +1059,7 @@ int lmgc_model_tensor_info(const lmgc_model_config* cfg, int32_t index, char* na
 
 int lmgc_model_create(const lmgc_model_config* cfg, const void* const* d_weights, void* stream, lmgc_model** out) {
   clear_error();
-  return create_model(cfg, d_weights, (hipStream_t)stream, out);
+  return guarded([&] { return create_model(cfg, d_weights, (hipStream_t)stream, out); });
 }
 
 void lmgc_model_destroy(lmgc_model* m) { delete m; }
@@ -1055,7 +1072,7 @@ size_t lmgc_probs_workspace(const lmgc_model* m, int32_t B, int32_t W) {
 int lmgc_probs(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t W, const lmgc_serial_params* p,
                uint32_t total, uint32_t* d_cdf, float* d_logp, void* d_ws, size_t ws_bytes, void* stream) {
   clear_error();
-  return run_probs(m, d_tokens, B, W, p, total, d_cdf, d_logp, d_ws, ws_bytes, (hipStream_t)stream);
+  return guarded([&] { return run_probs(m, d_tokens, B, W, p, total, d_cdf, d_logp, d_ws, ws_bytes, (hipStream_t)stream); });
 }
 
 size_t lmgc_encode_bound(int32_t n_win, int32_t W) {
@@ -1069,7 +1086,7 @@ int lmgc_encode(const uint32_t* cdf, int32_t nsym, const uint8_t* sym, const int
   if (nsym < 2 || nsym > 256 || n_win < 0 || W <= 0 || !used || (n_win > 0 && (!cdf || !sym || !len || !bits)))
     return set_error(LMGC_EINVAL, "lmgc_encode: bad arguments");
   if (n_win > 0 && !out) return set_error(LMGC_EINVAL, "lmgc_encode: NULL output");
-  return encode_windows(cdf, nsym, sym, len, n_win, W, out, cap, bits, used, n_threads);
+  return guarded([&] { return encode_windows(cdf, nsym, sym, len, n_win, W, out, cap, bits, used, n_threads); });
 }
 
 int lmgc_decode_init(lmgc_decoder* st, const uint8_t* payload, uint64_t nbits) {
@@ -1106,21 +1123,23 @@ int lmgc_probs_stepwise(const lmgc_model* m, const int32_t* d_tokens, int32_t B,
                         const lmgc_serial_params* p, uint32_t total, uint32_t* d_cdf, float* d_logp, void* d_ws,
                         size_t ws_bytes, void* stream) {
   clear_error();
-  return run_stepwise(m, d_tokens, B, W, p, total, d_cdf, d_logp, d_ws, ws_bytes, (hipStream_t)stream);
+  return guarded([&] { return run_stepwise(m, d_tokens, B, W, p, total, d_cdf, d_logp, d_ws, ws_bytes, (hipStream_t)stream); });
 }
 
 int lmgc_compress(const lmgc_model* m, const void* d_values, int64_t n_values, const lmgc_serial_params* p,
                   uint32_t total, int32_t batch, uint64_t model_tag, int64_t first_window, int64_t n_windows,
                   void* d_ws, size_t ws_bytes, uint8_t* out, size_t cap, size_t* used, void* stream) {
   clear_error();
-  return compress(m, d_values, n_values, p, total, batch, model_tag, first_window, n_windows, d_ws, ws_bytes, out,
-                  cap, used, (hipStream_t)stream);
+  return guarded([&] {
+    return compress(m, d_values, n_values, p, total, batch, model_tag, first_window, n_windows, d_ws, ws_bytes, out,
+                    cap, used, (hipStream_t)stream);
+  });
 }
 
 int lmgc_decode(const lmgc_model* m, const uint8_t* container, size_t bytes, int32_t batch, uint64_t expect_tag,
                 void* d_ws, size_t ws_bytes, void* values_out, void* stream) {
   clear_error();
-  return decode(m, container, bytes, batch, expect_tag, d_ws, ws_bytes, values_out, (hipStream_t)stream);
+  return guarded([&] { return decode(m, container, bytes, batch, expect_tag, d_ws, ws_bytes, values_out, (hipStream_t)stream); });
 }
 
 int lmgc_container_info(const uint8_t* container, size_t bytes, int64_t* n_values, int32_t* bytes_per_value,
@@ -1164,6 +1183,7 @@ int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint1
 }
 
 int lmgc_timing_enable(int32_t enable) {
+  return guarded([&] {
   std::lock_guard<std::mutex> g(g_timing.mu);
   g_timing.on = enable != 0;
   for (int k = 0; k < LMGC_K_COUNT; k++) {
@@ -1177,6 +1197,7 @@ int lmgc_timing_enable(int32_t enable) {
     g_timing.count[k] = 0;
   }
   return LMGC_OK;
+  });
 }
 
 int lmgc_timing_kinds(uint32_t kind_mask) {
@@ -1189,6 +1210,7 @@ int lmgc_timing_kinds(uint32_t kind_mask) {
 
 int lmgc_timing_read(int32_t kind, double* total_ms, int64_t* count) {
   if (kind < 0 || kind >= LMGC_K_COUNT) return set_error(LMGC_EINVAL, "bad kernel kind");
+  return guarded([&] {
   std::lock_guard<std::mutex> g(g_timing.mu);
   for (int k = 0; k < LMGC_K_COUNT; k++) {
     for (auto& pr : g_timing.pending[k]) {
@@ -1205,6 +1227,7 @@ int lmgc_timing_read(int32_t kind, double* total_ms, int64_t* count) {
   if (total_ms) *total_ms = g_timing.ms[kind];
   if (count) *count = g_timing.count[kind];
   return LMGC_OK;
+  });
 }
 
 double lmgc_probs_flops(const lmgc_model* m, int32_t B, int32_t W, int32_t kind) {

@@ -11,6 +11,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <system_error>
 #include <thread>
 #include <vector>
 
@@ -165,7 +166,14 @@ int encode_windows(const uint32_t* cdf, int nsym, const uint8_t* sym, const int3
   int T = n_threads > 0 ? n_threads : (int)std::min(8u, std::max(1u, std::thread::hardware_concurrency()));
   T = std::min(T, n_win);
   std::vector<std::thread> pool;
-  for (int t = 1; t < T; t++) pool.emplace_back(worker);
+  pool.reserve(T);  // no reallocation below, so only a thread start can fail
+  for (int t = 1; t < T; t++) {
+    try {
+      pool.emplace_back(worker);
+    } catch (const std::system_error&) {
+      break;  // run with the threads that did start
+    }
+  }
   worker();
   for (auto& th : pool) th.join();
   if (err.load()) {

@@ -303,3 +303,21 @@ def test_size_limits_and_hostile_headers():
     with pytest.raises(B.LMGCError) as e:
         B.container_info(bytes(bad))
     assert e.value.code == -5
+
+
+def test_host_allocation_failure_is_an_error_code():
+    """A host allocation that cannot succeed (the encoder's scratch for 2^31
+    windows of 2^20 tokens, about a petabyte, beyond the address space)
+    comes back as LMGC_ENOMEM, not as an exception through the C ABI."""
+    import ctypes
+    cdf = np.zeros(19, np.uint32)
+    sym = np.zeros(1, np.uint8)
+    lens = np.zeros(1, np.int32)
+    out = np.zeros(16, np.uint8)
+    bits = np.zeros(1, np.uint32)
+    used = ctypes.c_size_t()
+    rc = B.lib().lmgc_encode(cdf.ctypes.data, 18, sym.ctypes.data, lens.ctypes.data, (1 << 31) - 1,
+                             1 << 20, out.ctypes.data, out.size, bits.ctypes.data,
+                             ctypes.byref(used), 1)
+    assert rc == -2, rc  # LMGC_ENOMEM
+    assert b"allocation" in B.lib().lmgc_last_error()
