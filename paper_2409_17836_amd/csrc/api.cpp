@@ -291,11 +291,17 @@ static int create_model(const lmgc_model_config* cfg, const void* const* w, hipS
   m->d_pad = (int)round_up(d, m->tile);
   m->v_pad = (int)round_up(c.vocab, m->tile);
   std::vector<void*> temps;
-  auto fail = [&](int code) {
-    for (void* p : temps) hipFree(p);
-    delete m;
-    return code;
-  };
+  // Frees the repack temporaries on every exit, and the model too unless it
+  // was handed out (also when a host allocation throws).
+  struct Cleanup {
+    std::vector<void*>& temps;
+    lmgc_model*& m;
+    ~Cleanup() {
+      for (void* p : temps) hipFree(p);
+      delete m;
+    }
+  } cleanup{temps, m};
+  auto fail = [](int code) { return code; };
   auto vec_bytes = [&](int64_t n) { return (size_t)n * m->act; };
   size_t k = 0;  // manifest cursor
   if (c.arch == LMGC_ARCH_LLAMA) {
@@ -381,8 +387,8 @@ static int create_model(const lmgc_model_config* cfg, const void* const* w, hipS
       return fail(rc);
   }
   if (hipStreamSynchronize(s) != hipSuccess) return fail(set_error(LMGC_EDEVICE, "model repack failed"));
-  for (void* p : temps) hipFree(p);
   *out = m;
+  m = nullptr;  // owned by the caller now
   return LMGC_OK;
 }
 
