@@ -123,6 +123,30 @@ def copy_calibration(mib):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "copies": 3}), flush=True)
 
 
+def decode_bench(B, model, dv, sp, Bw, W, name):
+    """The decoder's path: lmgc_probs_stepwise computes the tables one
+    position at a time through the K/V cache, all Bw windows of the batch per
+    token step, as lmgc_decode does between its host decoding steps.  Timed
+    over whole windows of W positions; the tables are checked bit for bit
+    against lmgc_probs (the encoder's), which lossless decoding needs."""
+    import torch
+    tok, _ = B.serialize(dv, sp, 0, Bw)
+    B.probs_stepwise(model, tok[:, :64].contiguous(), sp)  # warm-up
+    ws = B.workspace(model.step_workspace(Bw, W), tok.device)
+    torch.cuda.synchronize()
+    log(f"[bench] decoding path: {W} token steps of {Bw} windows")
+    t0 = time.perf_counter()
+    cdf1, lp1 = B.probs_stepwise(model, tok, sp, ws=ws)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    cdf0, lp0 = B.probs(model, tok, sp)
+    same = bool(torch.equal(cdf0, cdf1)) and bool(torch.equal(lp0.view(torch.int32), lp1.view(torch.int32)))
+    print(json.dumps({"metric": "decoding path, ms per token step (all windows of the batch)",
+                      "value": round(dt * 1e3 / W, 4), "unit": "ms", "higher_is_better": False,
+                      "workload": name, "windows": Bw, "window_tokens": W, "token_steps": W,
+                      "tables_bit_identical_to_encoder": same}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -137,6 +161,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-values", type=int, default=2)
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_gemm_up_7b.json"))
+    ap.add_argument("--decode", action="store_true",
+                    help="time the decoding path (per-position tables through the K/V cache) instead")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run plain copies of this size (counter calibration)")
     args = ap.parse_args()
@@ -195,6 +221,9 @@ def main():
         torch.cuda.synchronize()
         lossy_ms = (time.perf_counter() - t0) * 1e3
         log(f"[bench] lossy steps {w.lossy}: {lossy_ms:.2f} ms for {w.n_values} values")
+    if args.decode:
+        decode_bench(B, model, dv, sp, Bw, W, w.name)
+        return
     n_vals = dv.numel()
     n_win = B.num_windows(n_vals, sp)
     need = (args.warmup + args.steps) * Bw
