@@ -396,7 +396,8 @@ static int create_model(const lmgc_model_config* cfg, const void* const* w, hipS
 struct ProbsWs {
   float* h;
   void *a, *q, *k, *v, *o, *ff;
-  float* logits;
+  float* za;         // [M, LMGC_NALPHA_MAX] alphabet logits
+  float2* part;      // [M, v_pad / 64] log-sum-exp partials of the LM head
   void* head_alpha;  // [tile, d] alphabet rows of the LM head (renormalised tables)
   size_t bytes;
 };
@@ -418,13 +419,13 @@ static ProbsWs carve(const lmgc_model* m, int B, int W, char* base) {
   w.v = take(M * c.n_kv_heads * m->hd * m->act);
   w.o = take(M * c.n_heads * m->hd * m->act);
   w.ff = take(M * c.d_ff * m->act);
-  w.logits = (float*)take(M * m->v_pad * 4);
+  w.za = (float*)take(M * LMGC_NALPHA_MAX * 4);
+  w.part = (float2*)take(M * (m->v_pad / 64) * sizeof(float2));
   w.head_alpha = take((size_t)m->tile * c.d_model * m->act);
   w.bytes = off;
   return w;
 }
 
-// ---------------------------------------------------------------- forward
 // ---------------------------------------------------------------- forward
 // Activation buffers of one forward pass.  kc[l] / vc[l]: layer l's K and V
 // (V^T for bf16 models) in [B, Hkv, W, hd] ([B, Hkv, hd, W]) layout; a batch
@@ -433,7 +434,8 @@ static ProbsWs carve(const lmgc_model* m, int B, int W, char* base) {
 struct FwdBufs {
   float* h;
   void *a, *q, *o, *ff;
-  float* logits;
+  float* za;
+  float2* part;
   void* head_alpha;
   void* const* kc;
   void* const* vc;
@@ -537,41 +539,42 @@ static int forward(const lmgc_model* m, const int32_t* tok, int B, int W, int dp
     ScopedTimer t(LMGC_K_NORM, s);
     HIP_OK(launch_norm(f.h, M, d, m->final_g, m->final_b, !llama, c.norm_eps, c.dtype, f.a, s));
   }
+  // LM head (Sec. 4, "Compression": the coder's distribution is the LM's
+  // softmax over the whole vocabulary).  The logits stay in registers: the
+  // head GEMM's epilogue writes each row's log-sum-exp partial per 64-column
+  // group and the alphabet logits, and launch_head_tables merges the
+  // partials in a fixed order into the LSE and quantises the table.
   int32_t ids[LMGC_NALPHA_MAX];
   const int na = alphabet(*p, ids);
+  EpiArgs e = {};
+  e.kind = EPI_HEAD;
+  e.M = M;
+  e.za = f.za;
+  e.ld_za = LMGC_NALPHA_MAX;
+  e.n_alpha = na;
   if (p->renorm) {
     // Renormalised tables need only the alphabet's logits: the LM head is
-    // cut to its A alphabet rows (one N tile), and the LSE runs over them.
-    int32_t compact[LMGC_NALPHA_MAX];
-    for (int a = 0; a < na; a++) compact[a] = a;
-    {
-      ScopedTimer t(LMGC_K_GEMM_HEAD, s);
-      HIP_OK(launch_alpha_head(m->head, ids, na, m->tile, d, m->act, f.head_alpha, s));
-      EpiArgs e = {};
-      e.kind = EPI_STORE_F32;
-      e.M = M;
-      e.N = na;
-      e.c = f.logits;
-      e.ldc = m->tile;
-      HIP_OK(gemm(f.a, f.head_alpha, m->tile, d, e));
-    }
-    ScopedTimer t(LMGC_K_LSE_CDF, s);
-    HIP_OK(launch_lse_cdf(f.logits, M, m->tile, na, compact, na, total, 1, cdf, logp, s));
-    return LMGC_OK;
-  }
-  {
+    // cut to its A alphabet rows (one N tile, columns 0..A-1), and the LSE
+    // runs over them.
     ScopedTimer t(LMGC_K_GEMM_HEAD, s);
-    EpiArgs e = {};
-    e.kind = EPI_STORE_F32;
-    e.M = M;
+    HIP_OK(launch_alpha_head(m->head, ids, na, m->tile, d, m->act, f.head_alpha, s));
+    for (int a = 0; a < na; a++) e.alpha_ids[a] = a;
+    e.N = na;
+    e.part = nullptr;
+    e.ngroups = m->tile / 64;
+    HIP_OK(gemm(f.a, f.head_alpha, m->tile, d, e));
+  } else {
+    ScopedTimer t(LMGC_K_GEMM_HEAD, s);
+    for (int a = 0; a < na; a++) e.alpha_ids[a] = ids[a];
     e.N = c.vocab;
-    e.c = f.logits;
-    e.ldc = m->v_pad;
+    e.part = f.part;
+    e.ngroups = m->v_pad / 64;
     HIP_OK(gemm(f.a, m->head, m->v_pad, d, e));
   }
   {
     ScopedTimer t(LMGC_K_LSE_CDF, s);
-    HIP_OK(launch_lse_cdf(f.logits, M, m->v_pad, c.vocab, ids, na, total, 0, cdf, logp, s));
+    HIP_OK(launch_head_tables(f.part, m->v_pad / 64, f.za, LMGC_NALPHA_MAX, M, na, total, p->renorm, cdf,
+                              logp, s));
   }
   return LMGC_OK;
 }
@@ -592,7 +595,7 @@ static int run_probs(const lmgc_model* m, const int32_t* tok, int B, int W, cons
   if (ws_bytes < w.bytes) return set_error(LMGC_ESIZE, "workspace too small: %zu < %zu", ws_bytes, w.bytes);
 
   std::vector<void*> kc(c.n_layers, w.k), vc(c.n_layers, w.v);
-  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.logits, w.head_alpha, kc.data(), vc.data()};
+  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.za, w.part, w.head_alpha, kc.data(), vc.data()};
   return forward(m, tok, B, W, -1, p, total, f, cdf, logp, s);
 }
 
@@ -621,7 +624,8 @@ constexpr int kStepMaxB = 16;
 struct StepWs {
   float* h;
   void *a, *q, *o, *ff;
-  float* logits;
+  float* za;         // [B, LMGC_NALPHA_MAX] alphabet logits
+  float2* part;      // [B, v_pad / 64] log-sum-exp partials of the LM head
   void* head_alpha;  // [tile, d] alphabet rows of the LM head (renormalised tables)
   int32_t* tok;     // [B] input token of the step (the previous position's)
   uint32_t* cdf;    // [B, A + 2] (A: alphabet size)
@@ -645,7 +649,8 @@ static StepWs carve_step(const lmgc_model* m, int B, int W, char* base) {
   w.a = take((size_t)B * std::max<size_t>(c.d_model, hq) * act);
   w.o = take((size_t)B * hq * act);
   w.ff = take((size_t)B * c.d_ff * act);
-  w.logits = (float*)take((size_t)B * m->v_pad * 4);
+  w.za = (float*)take((size_t)B * LMGC_NALPHA_MAX * 4);
+  w.part = (float2*)take((size_t)B * (m->v_pad / 64) * sizeof(float2));
   w.head_alpha = take((size_t)m->tile * c.d_model * act);
   w.tok = (int32_t*)take((size_t)B * 4);
   w.cdf = (uint32_t*)take((size_t)B * (LMGC_NSYM_MAX + 1) * 4);
@@ -677,7 +682,7 @@ static int check_step(const lmgc_model* m, int B, int W, const lmgc_serial_param
 // the tokens at j - 1); tables land in w.cdf (and w.logp).
 static int run_step(const lmgc_model* m, StepWs& w, int B, int W, int j, const lmgc_serial_params* p,
                     uint32_t total, bool want_logp, hipStream_t s) {
-  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.logits, w.head_alpha, w.kc.data(), w.vc.data()};
+  const FwdBufs f = {w.h, w.a, w.q, w.o, w.ff, w.za, w.part, w.head_alpha, w.kc.data(), w.vc.data()};
   return forward(m, w.tok, B, W, j, p, total, f, w.cdf, want_logp ? w.logp : nullptr, s);
 }
 

@@ -35,6 +35,8 @@ enum EpiKind : int {
   EPI_QKV_BIAS = 3,    // + bias, scatter to q, k, v (no RoPE)       (act)
   EPI_SWIGLU = 4,      // out[row, f] = silu(gate) * up              (act)
   EPI_BIAS_GELU = 5,   // out[row, col] = gelu_tanh(v + bias[col])   (act)
+  EPI_HEAD = 6,        // LM head: per-(row, 64-column group) max and
+                       // sum of exp, and the alphabet columns' logits (float)
 };
 
 // Arguments of every epilogue (unused fields ignored).
@@ -59,6 +61,15 @@ struct EpiArgs {
   // SWIGLU / GELU output
   void* out;           // [M, ld_out]
   int ld_out;
+  // HEAD: za[row, a] = logit of column alpha_ids[a] (a < n_alpha); part[row,
+  // g] = (max, sum of exp(z - max)) over the valid columns of group g
+  // (columns 64 g .. 64 g + 63), nullable; ngroups = padded N / 64
+  float* za;
+  int ld_za;
+  float2* part;
+  int ngroups;
+  int n_alpha;
+  int alpha_ids[LMGC_NALPHA_MAX];
 };
 
 // ------------------------------------------------------------ launchers
@@ -110,12 +121,15 @@ hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uin
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,
                                 int B, int Hq, int Hkv, int W, int hd, int dq, hipStream_t s);
 
-// logits [M, ldz] (first V valid) -> cdf [M, A + 2], logp [M, A] (nullable);
-// alpha_ids is a host array of the A = n_alpha (17 or 18) alphabet token ids.
-// renorm: tables renormalised over the alphabet (the logits are then the
-// alphabet's own, V = A); otherwise full-vocabulary tables with an escape bin.
-hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
-                          int n_alpha, uint32_t total, int renorm, uint32_t* cdf, float* logp, hipStream_t s);
+// The LM head's tables from what its EPI_HEAD epilogue wrote: the partials
+// part [M, ngroups] merge, in a fixed order, into the row's log-sum-exp over
+// the whole vocabulary; za [M, ld_za] holds the n_alpha (17 or 18) alphabet
+// logits.  -> cdf [M, A + 2], logp [M, A] (nullable).  renorm: the tables
+// are renormalised over the alphabet (the log-sum-exp runs over za alone,
+// part is not read); otherwise full-vocabulary tables with an escape bin.
+hipError_t launch_head_tables(const float2* part, int ngroups, const float* za, int ld_za, int M,
+                              int n_alpha, uint32_t total, int renorm, uint32_t* cdf, float* logp,
+                              hipStream_t s);
 
 // dst [rows, cols]: row r < n_alpha = head row alpha_ids[r] (host array),
 // the remaining rows zero.  Rows are cols * elem_bytes bytes (multiple of 4).

@@ -1,6 +1,7 @@
 // Row-wise kernels of the decoder: embedding with the BOS shift, RMSNorm /
-// LayerNorm, the log-sum-exp + integer-table kernel at the LM head, and the
-// row gather used to repack weights.  All are HBM-bound; each uses one
+// LayerNorm, the kernel that turns the LM head's partials into log-sum-exp
+// and integer tables, and the row gather used to repack weights.  All are
+// HBM-bound; each uses one
 // 64-wide wavefront per row with fixed-order (butterfly) reductions, so every
 // row's result is a bitwise function of that row alone.
 #include <math.h>
@@ -166,58 +167,63 @@ __global__ void norm_bf16x4_kernel(const float* __restrict__ h, int M, const uin
 }
 
 // ------------------------------------------------------------ LSE + table
-// One wave per row: online max / sum-exp over the V logits, then the NA
-// alphabet log-probabilities and their integer table of NA + 2 entries
-// (quantised in double; escape bin NA).  renorm: the V logits are the
-// alphabet's own (V = NA), so the log-probabilities are normalised over the
-// alphabet; the largest frequency takes total - sum and the escape bin is
-// empty.
+// log-sum-exp merge of (m, s) with (mo, so): the larger maximum stays, the
+// other sum is rescaled; an empty side (m = -inf, s = 0) adds nothing.
+__device__ inline void lse_merge(float& m, float& s, float mo, float so) {
+  const float mn = fmaxf(m, mo);
+  if (mn == -INFINITY) return;
+  const float a = (m == -INFINITY) ? 0.f : s * expf(m - mn);
+  const float c = (mo == -INFINITY) ? 0.f : so * expf(mo - mn);
+  s = a + c;  // commutative: both sides of a butterfly get the same bits
+  m = mn;
+}
+
+// One wave per row.  Full-vocabulary tables: the row's head partials (one
+// (max, sum-exp) per 64-column group, written by the head GEMM's epilogue)
+// are merged lane-locally in group order (lane l: groups l, l + 64, ...),
+// then across the wave by a fixed butterfly; LSE = max + log(sum).
+// renorm: the log-sum-exp runs over the NA alphabet logits alone.  Then the
+// NA alphabet log-probabilities z_a - LSE and their integer table of NA + 2
+// entries (quantised in double; escape bin NA; renorm: the largest frequency
+// takes total - sum and the escape bin is empty).
 template <int NA>
-__global__ void lse_cdf_kernel(const float* __restrict__ z, int M, int ldz, int V,
-                               AlphaIds ids, uint32_t total, int renorm,
-                               uint32_t* __restrict__ cdf, float* __restrict__ logp) {
+__global__ void head_tables_kernel(const float2* __restrict__ part, int ngroups,
+                                   const float* __restrict__ za, int ld_za, int M, uint32_t total,
+                                   int renorm, uint32_t* __restrict__ cdf, float* __restrict__ logp) {
   constexpr int NS = NA + 1;  // coder bins incl. escape
   const uint32_t spread = renorm ? total - NA : total - NS;
   const int64_t alpha_total = renorm ? (int64_t)total : (int64_t)total - 1;
   const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (row >= M) return;
-  const float* zr = z + row * (int64_t)ldz;
+  const float* zr = za + row * (int64_t)ld_za;
   float m = -INFINITY, s = 0.f;
-  const int V4 = V & ~3;
-  // (unrolled so that several loads are in flight: a few rows, as in a
-  // decoding step, are bound by load latency; the per-lane order of the
-  // arithmetic is unchanged)
-#pragma unroll 8
-  for (int c = lane * 4; c < V4; c += kWave * 4) {
-    const float4 t = *reinterpret_cast<const float4*>(zr + c);
-    const float mx = fmaxf(fmaxf(t.x, t.y), fmaxf(t.z, t.w));
-    const float mn = fmaxf(m, mx);
-    s = s * expf(m - mn) + ((expf(t.x - mn) + expf(t.y - mn)) + (expf(t.z - mn) + expf(t.w - mn)));
-    m = mn;
+  if (renorm) {
+    if (lane < NA) {
+      m = zr[lane];
+      s = 1.f;
+    }
+  } else {
+    const float2* pr = part + row * (int64_t)ngroups;
+    // (unrolled so that several loads are in flight: the few rows of a
+    // decoding step are bound by load latency; the order of the merges is
+    // unchanged)
+#pragma unroll 4
+    for (int g = lane; g < ngroups; g += kWave) {
+      const float2 p = pr[g];
+      lse_merge(m, s, p.x, p.y);
+    }
   }
-  for (int c = V4 + lane; c < V; c += kWave) {
-    const float t = zr[c];
-    const float mn = fmaxf(m, t);
-    s = s * expf(m - mn) + expf(t - mn);
-    m = mn;
-  }
-  // merge (m, s) across the wave in a fixed butterfly
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
     const float mo = __shfl_xor(m, o, kWave);
     const float so = __shfl_xor(s, o, kWave);
-    const float mn = fmaxf(m, mo);
-    const float a = (m == -INFINITY) ? 0.f : s * expf(m - mn);
-    const float c = (mo == -INFINITY) ? 0.f : so * expf(mo - mn);
-    s = a + c;  // commutative: every lane gets the same bits
-    m = mn;
+    lse_merge(m, s, mo, so);
   }
   const float lse = m + logf(s);
   uint32_t f = 0;
-  float lp = 0.f;
   if (lane < NA) {
-    lp = zr[ids.v[lane]] - lse;
+    const float lp = zr[lane] - lse;
     const double p = exp((double)lp);
     f = 1u + (uint32_t)floor(p * (double)spread);
     if (logp) logp[row * NA + lane] = lp;
@@ -363,19 +369,19 @@ hipError_t launch_norm(const float* h, int M, int d, const void* gain, const voi
   return hipGetLastError();
 }
 
-hipError_t launch_lse_cdf(const float* logits, int M, int ldz, int V, const int32_t* alpha_ids,
-                          int n_alpha, uint32_t total, int renorm, uint32_t* cdf, float* logp,
-                          hipStream_t s) {
-  AlphaIds ids = {};
+hipError_t launch_head_tables(const float2* part, int ngroups, const float* za, int ld_za, int M,
+                              int n_alpha, uint32_t total, int renorm, uint32_t* cdf, float* logp,
+                              hipStream_t s) {
+  if (M <= 0) return hipSuccess;
   if (n_alpha != LMGC_NALPHA && n_alpha != LMGC_NALPHA_MAX) return hipErrorInvalidValue;
-  for (int a = 0; a < n_alpha; a++) ids.v[a] = alpha_ids[a];
+  if (ld_za < n_alpha || (!renorm && (!part || ngroups <= 0))) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((M + 3) / 4)), block(256);
   if (n_alpha == LMGC_NALPHA)
-    hipLaunchKernelGGL(lse_cdf_kernel<LMGC_NALPHA>, grid, block, 0, s, logits, M, ldz, V, ids, total, renorm, cdf,
-                       logp);
+    hipLaunchKernelGGL(head_tables_kernel<LMGC_NALPHA>, grid, block, 0, s, part, ngroups, za, ld_za, M, total,
+                       renorm, cdf, logp);
   else
-    hipLaunchKernelGGL(lse_cdf_kernel<LMGC_NALPHA_MAX>, grid, block, 0, s, logits, M, ldz, V, ids, total, renorm,
-                       cdf, logp);
+    hipLaunchKernelGGL(head_tables_kernel<LMGC_NALPHA_MAX>, grid, block, 0, s, part, ngroups, za, ld_za, M,
+                       total, renorm, cdf, logp);
   return hipGetLastError();
 }
 

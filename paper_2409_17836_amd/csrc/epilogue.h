@@ -64,6 +64,56 @@ __device__ inline void rope_rot(float vlo, float vhi, float c, float s, float& l
   hi = __builtin_fmaf(vhi, c, vlo * s);
 }
 
+// ------------------------------------------------------------- LM head
+// The head never stores its logits.  For every row and group of 64 columns
+// it writes the log-sum-exp partial (max m, sum of exp(z - m)) and the
+// logits of the alphabet columns; launch_head_tables merges the partials.
+// In all three matrix kernels (tiled bf16, decoding-step bf16, float32) a
+// group's 64 values of one row sit in 16 lanes of a wave, lane t holding
+// columns t + 16 j, j = 0..3, so one function reduces them for all three
+// and the encoder's and decoder's tables agree bit for bit.
+constexpr float kLog2e = 1.4426950408889634f;
+
+// z[j]: column t + 16 j of the group (-inf past the vocabulary).  The max
+// over the group, then exp(z - max) summed lane-locally in j order and over
+// the 16 lanes by a butterfly (xor 8, 4, 2, 1); max and + are commutative,
+// so all 16 lanes end with the same bits.  Every lane of the wave must call
+// it (it shuffles).
+__device__ inline float2 group_lse_part(const float z[4]) {
+  float m = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  float s = 0.f;
+  if (m != -INFINITY) {
+#pragma unroll
+    for (int j = 0; j < 4; j++) s += __builtin_amdgcn_exp2f((z[j] - m) * kLog2e);
+  }
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  return make_float2(m, s);
+}
+
+// Alphabet index of a (valid) head column, or -1.
+__device__ inline int alpha_index(const EpiArgs& e, int col) {
+  int a = -1;
+#pragma unroll
+  for (int t = 0; t < LMGC_NALPHA_MAX; t++)
+    if (t < e.n_alpha && e.alpha_ids[t] == col) a = t;
+  return a;
+}
+
+// One row of the head epilogue: z[j] and aidx[j] for the lane's columns
+// t + 16 j of group g; lane16 = t.  store: the row is in range.
+__device__ inline void head_row(const EpiArgs& e, const float z[4], const int aidx[4], int64_t row,
+                                bool store, int g, int lane16) {
+  const float2 p = group_lse_part(z);
+  if (!store) return;
+  if (e.part && lane16 == 0) e.part[row * e.ngroups + g] = p;
+#pragma unroll
+  for (int j = 0; j < 4; j++)
+    if (aidx[j] >= 0) e.za[row * e.ld_za + aidx[j]] = z[j];
+}
+
 // Column info of one (col, col + 32) pair.
 struct ColInfo {
   int seg, head, i;     // QKV target of col: segment (0 q, 1 k, 2 v), head, dim

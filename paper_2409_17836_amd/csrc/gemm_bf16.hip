@@ -256,6 +256,29 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   using E = Epi<uint16_t, KIND, HD>;
   using Pre4 = typename E::Pre4;
   const int c0 = n0 + wn * 64 + (lane & 15);
+  if constexpr (KIND == EPI_HEAD) {
+    // the wave's 64 columns are group (n0 + 64 wn) / 64; lane holds columns
+    // c0 + 16 j of rows 4 kq + r of every 16-row block
+    const int g = (n0 + wn * 64) >> 6;
+    bool ok[4];
+    int aidx[4];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      ok[j] = c0 + 16 * j < e.N;
+      aidx[j] = ok[j] ? alpha_index(e, c0 + 16 * j) : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; i++)
+#pragma unroll
+      for (int r = 0; r < 4; r++) {
+        const int row = m0 + wm * 128 + 16 * i + 4 * kq + r;
+        float z[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++) z[j] = ok[j] ? acc[i][j][r] : -INFINITY;
+        head_row(e, z, aidx, row, row < M, g, lane & 15);
+      }
+    return;
+  }
   ColInfo ci0 = E::column(e, c0), ci1 = E::column(e, c0 + 16);
   if (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS) {
     // bf16 models have head_dim 64 or 128, so q, k and v and every head are
@@ -370,7 +393,9 @@ template <int KIND, int HD, int NWR>
 __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t* __restrict__ A,
                                                                   const uint16_t* __restrict__ Bw,
                                                                   int M, int K, EpiArgs e) {
-  __shared__ f32x4 part[NWR == 4 ? 2 : 1][64];  // accumulators handed to the pair's first block
+  // accumulators handed over: to the pair's first block (QKV: waves 2, 3 to
+  // 0, 1), or all to wave 0 (HEAD: waves 1..3, the group's blocks j = 1..3)
+  __shared__ f32x4 part[NWR == 4 ? 3 : 1][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int c;  // this wave's block
   if (NWR == 4) c = blockIdx.x * 64 + wave * 16;
@@ -436,6 +461,30 @@ __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t
         p[col] = resid_add(p[col], acc[i], bias);
       }
     }
+  } else if constexpr (KIND == EPI_HEAD) {
+    static_assert(NWR == 4, "the head's groups are 64 columns: four waves");
+    if (wave > 0) part[wave - 1][lane] = acc;
+    __syncthreads();
+    if (wave > 0) return;
+    f32x4 blk[4];
+    blk[0] = acc;
+#pragma unroll
+    for (int j = 1; j < 4; j++) blk[j] = part[j - 1][lane];
+    bool ok[4];
+    int aidx[4];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      ok[j] = col + 16 * j < e.N;
+      aidx[j] = ok[j] ? alpha_index(e, col + 16 * j) : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int row = 4 * kq + i;
+      float z[4];
+#pragma unroll
+      for (int j = 0; j < 4; j++) z[j] = ok[j] ? blk[j][i] : -INFINITY;
+      head_row(e, z, aidx, row, row < M, blockIdx.x, r);
+    }
   } else {
     constexpr int NH = NWR / 2;  // the second half of the waves hand over
     if (wave >= NH) part[wave - NH][lane] = acc;
@@ -456,7 +505,7 @@ hipError_t launch_rows_one(const uint16_t* A, const uint16_t* B, int M, int N_pa
                            const EpiArgs& e, hipStream_t s) {
   if constexpr (KIND == EPI_RESID) {
     hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 1>), dim3(N_pad / 16), dim3(64), 0, s, A, B, M, K, e);
-  } else if constexpr (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS) {
+  } else if constexpr (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS || KIND == EPI_HEAD) {
     hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 4>), dim3(N_pad / 64), dim3(256), 0, s, A, B, M, K, e);
   } else {
     hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 2>), dim3(N_pad / 32), dim3(128), 0, s, A, B, M, K, e);
@@ -479,8 +528,8 @@ hipError_t launch_rows_kind(const uint16_t* A, const uint16_t* B, int M, int N_p
     }
   } else {
     switch (e.kind) {
-      case EPI_STORE_F32:
-        return launch_rows_one<EPI_STORE_F32, 0>(A, B, M, N_pad, K, e, s);
+      case EPI_HEAD:
+        return launch_rows_one<EPI_HEAD, 0>(A, B, M, N_pad, K, e, s);
       case EPI_RESID:
         return launch_rows_one<EPI_RESID, 0>(A, B, M, N_pad, K, e, s);
       case EPI_SWIGLU:
@@ -534,6 +583,8 @@ hipError_t launch_kind(const uint16_t* A, const uint16_t* B, int M, int K, int n
     switch (e.kind) {
       case EPI_STORE_F32:
         return launch_one<EPI_STORE_F32, 0, true>(A, B, M, K, ntm, ntn, rb, e, s);
+      case EPI_HEAD:
+        return launch_one<EPI_HEAD, 0, true>(A, B, M, K, ntm, ntn, rb, e, s);
       case EPI_RESID:
         return launch_one<EPI_RESID, 0, true>(A, B, M, K, ntm, ntn, rb, e, s);
       case EPI_SWIGLU:

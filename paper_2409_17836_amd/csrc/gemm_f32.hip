@@ -55,6 +55,26 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
     }
     __syncthreads();
   }
+  if constexpr (KIND == EPI_HEAD) {
+    // the tile is one 64-column group; the 16 threads of a row (tx = lane & 15
+    // of one wave) hold its columns tx + 16 j
+    bool ok[4];
+    int aidx[4];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      ok[j] = n0 + tx + 16 * j < e.N;
+      aidx[j] = ok[j] ? alpha_index(e, n0 + tx + 16 * j) : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int row = m0 + ty * 4 + i;
+      float z[4];
+#pragma unroll
+      for (int j = 0; j < 4; j++) z[j] = ok[j] ? acc[i][j] : -INFINITY;
+      head_row(e, z, aidx, row, row < M, blockIdx.x, tx);
+    }
+    return;
+  }
   // thread columns tx + 16 j: pairs (tx, tx + 32) and (tx + 16, tx + 48)
   using E = Epi<float, KIND, 0>;
   const ColInfo ci0 = E::column(e, n0 + tx), ci1 = E::column(e, n0 + tx + 16);
@@ -94,6 +114,9 @@ hipError_t launch_gemm_f32(const float* A, const float* B, int M, int N_pad, int
       break;
     case EPI_BIAS_GELU:
       hipLaunchKernelGGL(gemm_f32_kernel<EPI_BIAS_GELU>, grid, block, 0, s, A, B, M, K, e);
+      break;
+    case EPI_HEAD:
+      hipLaunchKernelGGL(gemm_f32_kernel<EPI_HEAD>, grid, block, 0, s, A, B, M, K, e);
       break;
     default:
       return hipErrorInvalidValue;
