@@ -163,6 +163,23 @@ int lmgc_sparsify_topk(const float* d_values, int64_t n_values, int64_t k, float
                        void* d_workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * lmgc_sparsify_topk without a workspace argument and without allocating,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).  Same
+ * arguments, result (bit for bit) and errors as lmgc_sparsify_topk, whose
+ * kernels it runs.  The scratch is the library's own: a 32 KiB device array
+ * that every GPU the library runs on holds until the process ends, found on
+ * the caller's current device, which must be the device of the buffers and
+ * the stream.  The call allocates nothing (no hipMalloc, no host staging).
+ * Sizes: n_values in [0, 2^31 - 1], as for lmgc_sparsify_topk; the scratch
+ * does not grow with n_values (EINVAL beyond that range).  Calls that
+ * overlap on one GPU share the scratch and race: serialise them (one stream,
+ * or events).  Errors: EINVAL, ESIZE, EDEVICE.
+ */
+int lmgc_sparsify_topk_noalloc(const float* d_values, int64_t n_values, int64_t k, float* d_out,
+                               void* stream);
+
+/*
  * Linear quantisation (Sec. 5.4, Eq. 4) of d_values to bits-bit indices:
  * idx = round-half-even(((v - min) / (max - min)) * (2^bits - 1)), each
  * operation in float32 with one rounding and no fused multiply-add; min and

@@ -76,6 +76,7 @@ def lib():
         "lmgc_deserialize": (ctypes.c_int, [vp, i64, i64, P(SerialParams), vp]),
         "lmgc_lossy_workspace": (i64, [i64]),
         "lmgc_sparsify_topk": (ctypes.c_int, [vp, i64, i64, vp, vp, sz, vp]),
+        "lmgc_sparsify_topk_noalloc": (ctypes.c_int, [vp, i64, i64, vp, vp]),
         "lmgc_quantize_linear": (ctypes.c_int, [vp, i64, i32, vp, P(ctypes.c_float), vp, sz, vp]),
         "lmgc_sign_pack": (ctypes.c_int, [vp, i64, vp, vp]),
         "lmgc_model_num_tensors": (i32, [P(ModelConfig)]),
@@ -229,6 +230,17 @@ def sparsify_topk(values, k: int, out=None, ws=None, stream=None):
         ws = workspace(lossy_workspace(n), values.device)
     _check(lib().lmgc_sparsify_topk(_ptr(values), n, int(k), _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream)))
+    return out
+
+
+def sparsify_topk_noalloc(values, k: int, out, stream=None):
+    """sparsify_topk on the library's own device scratch: no workspace, and
+    the call allocates nothing (out must be given; it may be values)."""
+    import torch
+    assert values.dtype == torch.float32 and values.is_contiguous()
+    assert out.dtype == torch.float32 and out.numel() == values.numel()
+    _check(lib().lmgc_sparsify_topk_noalloc(_ptr(values), values.numel(), int(k), _ptr(out),
+                                            _stream(stream)))
     return out
 
 

@@ -987,18 +987,41 @@ int64_t lmgc_lossy_workspace(int64_t n_values) {
   return (int64_t)lossy_workspace_bytes();
 }
 
-int lmgc_sparsify_topk(const float* d_values, int64_t n_values, int64_t k, float* d_out, void* d_workspace,
-                       size_t workspace_bytes, void* stream) {
-  clear_error();
+static int check_topk(const float* d_values, int64_t n_values, int64_t k, const float* d_out) {
   int rc = check_lossy_vec(d_values, n_values, d_out);
   if (rc) return rc;
   if (k < 0) return set_error(LMGC_EINVAL, "k must be >= 0");
   if (d_out != d_values && n_values > 0 &&
       (const char*)d_out < (const char*)(d_values + n_values) && (const char*)d_values < (const char*)(d_out + n_values))
     return set_error(LMGC_EINVAL, "d_out overlaps d_values without being equal to it");
+  return LMGC_OK;
+}
+
+int lmgc_sparsify_topk(const float* d_values, int64_t n_values, int64_t k, float* d_out, void* d_workspace,
+                       size_t workspace_bytes, void* stream) {
+  clear_error();
+  int rc = check_topk(d_values, n_values, k, d_out);
+  if (rc) return rc;
   if (n_values == 0) return LMGC_OK;
   if (k > 0 && (rc = check_lossy_ws(d_workspace, workspace_bytes))) return rc;
   hipError_t e = launch_sparsify_topk(d_values, n_values, k, d_out, d_workspace, (hipStream_t)stream);
+  if (e != hipSuccess) return set_error(LMGC_EDEVICE, "sparsify launch: %s", hipGetErrorString(e));
+  return LMGC_OK;
+}
+
+int lmgc_sparsify_topk_noalloc(const float* d_values, int64_t n_values, int64_t k, float* d_out, void* stream) {
+  clear_error();
+  int rc = check_topk(d_values, n_values, k, d_out);
+  if (rc) return rc;
+  if (n_values == 0) return LMGC_OK;
+  void* ws = nullptr;
+  size_t cap = 0;
+  hipError_t e = lossy_scratch(&ws, &cap);
+  if (e != hipSuccess) return set_error(LMGC_EDEVICE, "library scratch: %s", hipGetErrorString(e));
+  if (lossy_workspace_bytes() > cap)
+    return set_error(LMGC_ESIZE, "top-k needs %zu bytes of scratch, the library holds %zu", lossy_workspace_bytes(),
+                     cap);
+  e = launch_sparsify_topk(d_values, n_values, k, d_out, ws, (hipStream_t)stream);
   if (e != hipSuccess) return set_error(LMGC_EDEVICE, "sparsify launch: %s", hipGetErrorString(e));
   return LMGC_OK;
 }

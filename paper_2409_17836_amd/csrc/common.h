@@ -149,6 +149,9 @@ hipError_t launch_sparsify_topk(const float* v, int64_t n, int64_t k, float* out
 // Writes the vector's LossyMinMax to res (device memory, e.g. lossy_minmax_slot(ws)).
 hipError_t launch_minmax(const float* v, int64_t n, void* ws, LossyMinMax* res, hipStream_t s);
 LossyMinMax* lossy_minmax_slot(void* ws);
+// Address (on the current device) and size of the library-owned device
+// scratch that lmgc_sparsify_topk_noalloc uses in place of a workspace.
+hipError_t lossy_scratch(void** ptr, size_t* bytes);
 hipError_t launch_quantize_linear(const float* v, int64_t n, int bits, float mn, float mx, void* idx,
                                   hipStream_t s);
 hipError_t launch_sign_pack(const float* v, int64_t n, uint8_t* out, hipStream_t s);

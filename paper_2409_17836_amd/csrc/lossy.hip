@@ -12,6 +12,8 @@
 // lowest indices are kept, which needs the count of such keys before each
 // element: a per-chunk count, then an ordered pass per chunk with a block
 // scan.
+#include <mutex>
+
 #include "common.h"
 
 namespace lmgc {
@@ -379,6 +381,40 @@ hipError_t launch_minmax(const float* v, int64_t n, void* ws, LossyMinMax* res, 
   hipLaunchKernelGGL(minmax_kernel, dim3(g), dim3(kThreads), 0, s, v, n, part);
   hipLaunchKernelGGL(minmax_final_kernel, dim3(1), dim3(kThreads), 0, s, (const LossyMinMax*)part, (int)g, res);
   return hipGetLastError();
+}
+
+// ------------------------------------------------ library-owned scratch
+// The scratch of lmgc_sparsify_topk_noalloc: a file-scope device array, one
+// copy on every GPU the library runs on, held from module load until the
+// process ends.  In host code `scratch` names a host-side stand-in, not a
+// device address; the current device's copy is found with
+// hipGetSymbolAddress (once per device, then cached) and only that address
+// reaches the kernels.  The top-k kernels clear what must start at zero
+// (state and histogram) themselves and write every tie count before reading
+// it, so what an earlier call left there does not matter; calls that overlap
+// on one GPU (two streams at once) race on it.
+constexpr size_t kScratchBytes = 32768;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+hipError_t lossy_scratch(void** ptr, size_t* bytes) {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  *bytes = kScratchBytes;
+  return hipSuccess;
 }
 
 LossyMinMax* lossy_minmax_slot(void* ws) {
