@@ -111,8 +111,12 @@ int64_t lmgc_num_tokens(int64_t n_values, const lmgc_serial_params* p);
 int64_t lmgc_num_windows(int64_t n_values, const lmgc_serial_params* p);
 
 /*
- * Serialise windows [first_window, first_window + n_windows) of the stream of
- * d_values (n_values values of bytes_per_value bytes, device memory).
+ * Serialisation (Sec. 4, "Serialization"): windows [first_window,
+ * first_window + n_windows) of the token stream of d_values (n_values values
+ * of bytes_per_value bytes, device memory).  A range rather than the whole
+ * stream, so that one batch of windows goes straight into the LM's input
+ * buffer; the whole stream is first_window = 0, n_windows =
+ * lmgc_num_windows(). d_tokens must be 16-byte and d_sym 4-byte aligned.
  *   d_tokens: [n_windows, W] int32 token ids; positions past the end of the
  *             stream get pad_id.
  *   d_sym:    nullable; [n_windows, W] uint8 coder bins (255 past the end).
@@ -123,8 +127,9 @@ int lmgc_serialize(const void* d_values, int64_t n_values, const lmgc_serial_par
                    uint8_t* d_sym, void* stream);
 
 /*
- * Host inverse on coder bins: sym[n_tokens] -> values_out (n_values *
- * bytes_per_value bytes).  ECORRUPT if a digit or separator is out of place,
+ * Host inverse of the serialisation (Sec. 4: decoding ends by mapping the
+ * decoded text back to the float32 values) on coder bins: sym[n_tokens] ->
+ * values_out (n_values * bytes_per_value bytes).  ECORRUPT if a digit or separator is out of place,
  * a bin is out of range or n_tokens does not match n_values.
  */
 int lmgc_deserialize(const uint8_t* sym, int64_t n_tokens, int64_t n_values,
@@ -141,6 +146,14 @@ int lmgc_deserialize(const uint8_t* sym, int64_t n_tokens, int64_t n_values,
  *
  * Device pointers must be 16-byte aligned; n_values <= 2^31 - 1.
  */
+
+/*
+ * Number of values sparsification keeps when it keeps `percent` percent of
+ * n_values values (Sec. 5.4 keeps 50, 25 and 10 percent):
+ * floor(n_values * percent / 100).  Returns < 0 if n_values is outside
+ * [0, 2^31 - 1] or percent outside [0, 100].  Host, pure arithmetic.
+ */
+int64_t lmgc_keep_count(int64_t n_values, int32_t percent);
 
 /* Device workspace bytes of lmgc_sparsify_topk and lmgc_quantize_linear
  * (a few tens of KiB, independent of n_values), or < 0 if n_values is bad. */
@@ -249,8 +262,11 @@ int lmgc_model_tensor_info(const lmgc_model_config* cfg, int32_t index, char* na
                            size_t name_cap, int32_t* ndim, int64_t shape[2]);
 
 /*
- * Create a model from device tensors in manifest order, each of the config's
- * dtype (bfloat16 bit patterns for BF16).  The handle copies and repacks
+ * The LLM that serves as the prior (Sec. 5.1 uses pretrained TinyLlama,
+ * OpenLLaMA and LLaMA-2; any weights of a supported shape work).  Create a
+ * model from device tensors in manifest order, each of the config's dtype
+ * (bfloat16 bit patterns for BF16); the caller loads them with any loader
+ * (no weight file format is defined here).  The handle copies and repacks
  * what it needs into its own device memory (the caller may free the inputs
  * after the call returns).  Synchronises `stream`.
  * Errors: EINVAL (bad config), ENOMEM, EDEVICE.
@@ -306,11 +322,13 @@ int lmgc_probs_stepwise(const lmgc_model* m, const int32_t* d_tokens, int32_t B,
  * most significant bit first and padded with zero bits to a whole byte.
  * Flush: pending+1 bits, the first 0 if low < 1/4 else 1.
  */
-/* Upper bound of the payload bytes lmgc_encode writes for these windows. */
+/* Upper bound of the payload bytes lmgc_encode writes for these windows
+ * (Sec. 3: at most 2 bits above the code length, per window). */
 size_t lmgc_encode_bound(int32_t n_win, int32_t W);
 
 /*
- * Host.  cdf: [n_win, W, nsym+1] uint32 tables (cdf[..., nsym] = total);
+ * Arithmetic encoding of windows with the LM's tables (Sec. 3; Sec. 4,
+ * "Compression").  Host.  cdf: [n_win, W, nsym+1] uint32 tables (cdf[..., nsym] = total);
  * sym: [n_win, W] bins; len[w] <= W symbols of window w are coded.
  * Writes the windows' payloads back to back into out (cap bytes); bits[w]
  * gets window w's exact bit count and *used the bytes written.
@@ -326,6 +344,10 @@ typedef struct {
   uint64_t opaque[8];
 } lmgc_decoder;
 
+/* Arithmetic decoding (Sec. 3), one symbol at a time, so that the table of
+ * the next position can be computed from the symbols decoded so far
+ * (Sec. 4, "Compression").  init: payload of nbits bits (bits past the end
+ * read as zero). */
 int lmgc_decode_init(lmgc_decoder* st, const uint8_t* payload, uint64_t nbits);
 /* Decode one symbol with model row cdf_row[nsym+1]; *sym_out gets the bin. */
 int lmgc_decode_symbol(lmgc_decoder* st, const uint32_t* cdf_row, int32_t nsym,
@@ -333,7 +355,10 @@ int lmgc_decode_symbol(lmgc_decoder* st, const uint32_t* cdf_row, int32_t nsym,
 
 /* -------------------------------------------------------------- container */
 /*
- * Container (little-endian): 128-byte header
+ * Container: what the compression rate of Eq. 3 counts (all its bytes).
+ * Windows are coded independently (Sec. 4: the stream is split into
+ * windows of the LM's context), so the header records each window's bit
+ * count.  Layout (little-endian): 128-byte header
  *   0 "LMGC" | 4 u16 version=1 | 6 u16 header bytes=128 | 8 u64 model tag |
  *   16 u64 n_values | 24 u8 bytes_per_value | 25 u8 bytes_per_group |
  *   26 u8 msb_first | 27 u8 nsym (A + 1) | 28 u32 W | 32 u32 total |
@@ -353,7 +378,8 @@ size_t lmgc_codec_workspace(const lmgc_model* m, int64_t n_values, const lmgc_se
                             int32_t batch);
 
 /*
- * Compress d_values (device) into a container at out (host).  Windows
+ * LM-GC compression (Sec. 4, Fig. 1: serialise, LM tables, arithmetic
+ * coding, per window).  Compress d_values (device) into a container at out (host).  Windows
  * [first_window, first_window + n_windows) are coded (n_windows < 0: all
  * windows from first_window on); the header records all of the vector's
  * windows only when the whole vector is coded.  batch windows per LM call;
@@ -367,8 +393,9 @@ int lmgc_compress(const lmgc_model* m, const void* d_values, int64_t n_values,
                   void* stream);
 
 /*
- * Decompress a whole-vector container into values_out (host, n_values *
- * bytes_per_value bytes).  Decodes groups of min(batch, 16) windows token by
+ * LM-GC decompression (Sec. 4, "Compression": the LM is replayed from BOS
+ * and each decoded token is fed back).  Decompress a whole-vector container
+ * into values_out (host, n_values * bytes_per_value bytes).  Decodes groups of min(batch, 16) windows token by
  * token from BOS: each step computes the next position's tables of the
  * group through the K/V cache (as lmgc_probs_stepwise, bit for bit the
  * encoder's tables), the host decodes one symbol per window and its token
@@ -380,7 +407,8 @@ int lmgc_decode(const lmgc_model* m, const uint8_t* container, size_t bytes, int
                 uint64_t expect_tag, void* d_ws, size_t ws_bytes, void* values_out,
                 void* stream);
 
-/* Parse a container header: n_values and windows, for sizing buffers. */
+/* Parse a container header (the layout above): n_values and windows, for
+ * sizing buffers.  Errors: ECORRUPT. */
 int lmgc_container_info(const uint8_t* container, size_t bytes, int64_t* n_values,
                         int32_t* bytes_per_value, int64_t* n_windows, uint64_t* model_tag);
 

@@ -29,8 +29,8 @@ standard LLaMA and GPT-2 block equations):
 Precision reading for bf16 models: weights are bf16 values; the operands of
 every matrix product (normed activations, q/k/v after RoPE, attention output,
 FFN activation, final normed state) are rounded to bf16; everything else
-(residual stream, norms, softmax, logits) is exact float64 here.  f32 models
-use no rounding.
+(residual stream, norms, the attention probabilities and their softmax,
+logits) is exact float64 here.  f32 models use no rounding.
 """
 from typing import Callable, Dict, Optional
 

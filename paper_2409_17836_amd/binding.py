@@ -74,6 +74,7 @@ def lib():
         "lmgc_num_windows": (i64, [i64, P(SerialParams)]),
         "lmgc_serialize": (ctypes.c_int, [vp, i64, P(SerialParams), i64, i64, vp, vp, vp]),
         "lmgc_deserialize": (ctypes.c_int, [vp, i64, i64, P(SerialParams), vp]),
+        "lmgc_keep_count": (i64, [i64, i32]),
         "lmgc_lossy_workspace": (i64, [i64]),
         "lmgc_sparsify_topk": (ctypes.c_int, [vp, i64, i64, vp, vp, sz, vp]),
         "lmgc_sparsify_topk_noalloc": (ctypes.c_int, [vp, i64, i64, vp, vp]),
@@ -211,6 +212,14 @@ def deserialize(sym: np.ndarray, n_values: int, sp: SerialParams, dtype) -> np.n
 
 
 # ------------------------------------------------------------ lossy steps --
+def keep_count(n_values: int, percent: int) -> int:
+    """Values sparsification keeps at `percent` percent (Sec. 5.4)."""
+    k = int(lib().lmgc_keep_count(n_values, percent))
+    if k < 0:
+        _check(k)
+    return k
+
+
 def lossy_workspace(n_values: int) -> int:
     n = int(lib().lmgc_lossy_workspace(n_values))
     if n < 0:
@@ -280,7 +289,7 @@ def lossy_prepare(values, steps, stream=None):
         if kind == "sparsify":
             if ws is None:
                 ws = workspace(lossy_workspace(x.numel()), x.device)
-            x = sparsify_topk(x, x.numel() * int(arg) // 100, ws=ws, stream=stream)
+            x = sparsify_topk(x, keep_count(x.numel(), int(arg)), ws=ws, stream=stream)
         elif kind == "quantize":
             if ws is None:
                 ws = workspace(lossy_workspace(x.numel()), x.device)

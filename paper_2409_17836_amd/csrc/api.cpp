@@ -981,6 +981,13 @@ static int check_lossy_ws(const void* ws, size_t bytes) {
   return LMGC_OK;
 }
 
+int64_t lmgc_keep_count(int64_t n_values, int32_t percent) {
+  clear_error();
+  if (n_values < 0 || n_values > INT32_MAX) return set_error(LMGC_EINVAL, "n_values must be in [0, 2^31 - 1]");
+  if (percent < 0 || percent > 100) return set_error(LMGC_EINVAL, "percent must be in [0, 100]");
+  return n_values * percent / 100;  // < 2^38: no overflow
+}
+
 int64_t lmgc_lossy_workspace(int64_t n_values) {
   clear_error();
   if (n_values < 0 || n_values > INT32_MAX) return set_error(LMGC_EINVAL, "n_values must be in [0, 2^31 - 1]");

@@ -321,3 +321,15 @@ def test_host_allocation_failure_is_an_error_code():
                              ctypes.byref(used), 1)
     assert rc == -2, rc  # LMGC_ENOMEM
     assert b"allocation" in B.lib().lmgc_last_error()
+
+
+def test_keep_count_matches_oracle():
+    """The Sec. 5.4 keep count is the library's arithmetic (the binding only
+    forwards it); it equals the oracle's floor(n * percent / 100)."""
+    from oracle import lossy as olossy
+    for n in (0, 1, 7, 99, 100, 101, 1 << 23, (1 << 31) - 1):
+        for pct in (0, 1, 10, 25, 33, 50, 99, 100):
+            assert B.keep_count(n, pct) == olossy.keep_count(n, pct)
+    for n, pct in ((-1, 10), (1 << 31, 10), (10, -1), (10, 101)):
+        with pytest.raises(B.LMGCError):
+            B.keep_count(n, pct)
