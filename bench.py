@@ -25,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 matrix peak
+PEAK_F32_VECTOR_TFLOPS = 157.3     # MI355X float32 vector peak (the tiny model's FMA kernels)
 DOMINANT = "gemm_up"               # gate/up projection + SwiGLU: 44% of the FLOPs
 
 
@@ -32,34 +33,82 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, host_weights, values, n_values_sample):
-    """Time the oracle (as it stands) compressing the first values of the
-    vector: one window prefix of the same workload."""
-    import numpy as np
+def cpu_info():
+    """nproc and the CPU model name of this host."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return os.cpu_count() or 1, model
 
+
+WHOLE_VECTOR_TOKENS = 1 << 16
+
+
+def cpu_baseline(w, host_weights, raw_values, all_positions=256, one_positions=32):
+    """The oracle as it stands, timed on this host's cores.  Its float64
+    weights are decoded once, outside the timed region.  Two legs, each
+    compressing a prefix of the workload's vector (window 0's first
+    positions; the whole vector if it is smaller): all cores on at least
+    `all_positions` tokens, one thread on at least `one_positions` tokens.
+    Lossy workloads run the oracle's own lossy steps on the raw vector first
+    (timed separately)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    from oracle import lossy as olossy
     from oracle import pipeline as opipe
     from oracle.forward import Model as OModel
+    from synth.gen import weight_manifest
 
-    om = OModel(w.model, host_weights)
-    sample = values[:n_values_sample]
+    nproc, cpu_model = cpu_info()
+    om = OModel(w.model, host_weights, cache=True)
     t0 = time.perf_counter()
-    buf = opipe.compress(sample, w.serial, om)
-    dt = time.perf_counter() - t0
-    threads = min(16, os.cpu_count() or 1)  # weight-decoding pool of the oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([threads] + [i.get("num_threads", 1) for i in threadpool_info()])
-    except ImportError:
-        pass
+    for name, _ in weight_manifest(w.model):
+        om.w(name)
+    decode_s = time.perf_counter() - t0
+    values, prep_s = raw_values, 0.0
+    if w.lossy:
+        t0 = time.perf_counter()
+        values = olossy.prepare(raw_values, w.lossy)
+        prep_s = time.perf_counter() - t0
+    tok_per_value = opipe.serialize(values[:64], w.serial)[0].size / min(64, values.size)
+    legs = {}
+    # a vector of at most WHOLE_VECTOR_TOKENS tokens (the tiny workload) is
+    # compressed whole on all cores
+    whole = values.size * tok_per_value <= WHOLE_VECTOR_TOKENS
+    for leg, positions, threads in (("all_cores", all_positions, None), ("one_thread", one_positions, 1)):
+        n = values.size if (whole and threads is None) else \
+            min(values.size, int(np.ceil(positions / tok_per_value)))
+        sample = values[:n]
+        with threadpool_limits(threads):
+            used = max([1] + [i.get("num_threads", 1) for i in threadpool_info()])
+            t0 = time.perf_counter()
+            buf = opipe.compress(sample, w.serial, om)
+            dt = time.perf_counter() - t0
+        ntok = opipe.serialize(sample, w.serial)[0].size
+        legs[leg] = {"threads": used, "values": int(n), "tokens": int(ntok), "seconds": round(dt, 2),
+                     "tokens_per_s": round(ntok / dt, 2),
+                     "grad_MB_per_s": sample.nbytes / dt / 1e6, "container_bytes": len(buf)}
+    a = legs["all_cores"]
     return {
-        "value": sample.nbytes / dt / 1e6,
+        "value": a["grad_MB_per_s"],
         "unit": "MB/s",
-        "cores": threads,
+        "cores": a["threads"],
         "kind": "oracle",
-        "sample": f"{n_values_sample} values = {9 * n_values_sample} tokens (a prefix of window 0) "
-                  f"through the float64 NumPy forward + quantiser + coder; {dt:.1f} s, "
-                  f"{len(buf)} bytes",
-        "seconds": dt,
+        "sample": f"{a['values']} values = {a['tokens']} tokens "
+                  f"({'the whole vector' if whole else 'window 0 prefix'}) through the float64 "
+                  f"NumPy forward + quantiser + coder on {a['threads']} threads in {a['seconds']} s; "
+                  f"weights decoded once beforehand ({decode_s:.1f} s, not timed)",
+        "tokens_per_s": a["tokens_per_s"],
+        "one_thread": legs["one_thread"],
+        "nproc": nproc,
+        "cpu_model": cpu_model,
+        "lossy_prep_s": round(prep_s, 2) if w.lossy else None,
     }
 
 
@@ -159,7 +208,11 @@ def main():
     ap.add_argument("--renorm", action="store_true",
                     help="tables renormalised over the alphabet (LM head cut to the alphabet)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-values", type=int, default=2)
+    ap.add_argument("--repeats", type=int, default=3, help="timed repeats of --steps steps (median reported)")
+    ap.add_argument("--cpu-positions", type=int, default=256,
+                    help="tokens of the oracle's all-core timing sample")
+    ap.add_argument("--cpu-positions-one", type=int, default=32,
+                    help="tokens of the oracle's one-thread timing sample")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_gemm_up_7b.json"))
     ap.add_argument("--decode", action="store_true",
                     help="time the decoding path (per-position tables through the K/V cache) instead")
@@ -226,55 +279,73 @@ def main():
         return
     n_vals = dv.numel()
     n_win = B.num_windows(n_vals, sp)
-    need = (args.warmup + args.steps) * Bw
-    assert need <= n_win, f"{need} windows needed, workload has {n_win}"
     ws = B.workspace(model.codec_workspace(n_vals, sp, Bw))
-    stream = torch.cuda.current_stream()
     log(f"[bench] model ready; warmup {args.warmup} step(s)")
+    # Window ranges: steps take consecutive batches of the vector's windows;
+    # a workload with fewer windows than the run needs (the tiny one is one
+    # batch) compresses the same batch in every step, one call per step.
+    per_call = (args.warmup + args.repeats * args.steps) * Bw <= n_win
+    reuse = not per_call
+
+    def run_steps(first_step, n_steps):
+        if per_call:
+            return B.compress(model, dv, sp, batch=Bw, first_window=first_step * Bw,
+                              n_windows=n_steps * Bw, ws=ws)
+        out = None
+        for _ in range(n_steps):
+            out = B.compress(model, dv, sp, batch=Bw, first_window=0, n_windows=min(Bw, n_win), ws=ws)
+        return out
 
     if args.warmup:
-        B.compress(model, dv, sp, batch=Bw, first_window=0, n_windows=args.warmup * Bw, ws=ws)
+        run_steps(0, args.warmup)
     torch.cuda.synchronize()
 
-    log(f"[bench] timing {args.steps} step(s)")
     # inside the timed region events are recorded only around the dominant
     # kernel's launches (each event pair adds a little time between launches)
     B.timing_kinds([DOMINANT])
     B.timing_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    buf = B.compress(model, dv, sp, batch=Bw, first_window=args.warmup * Bw,
-                     n_windows=args.steps * Bw, ws=ws)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
+    times = []
+    for r in range(args.repeats):
+        log(f"[bench] repeat {r + 1}/{args.repeats}: timing {args.steps} step(s)")
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        buf = run_steps(args.warmup + r * args.steps, args.steps)
+        torch.cuda.synchronize()
+        times.append(time.perf_counter() - t0)
     dom = B.timing_read(DOMINANT)
     B.timing_enable(False)
     # per-kernel breakdown from one more, untimed step with events on every kind
     B.timing_kinds(None)
     B.timing_enable(True)
-    B.compress(model, dv, sp, batch=Bw, first_window=0, n_windows=Bw, ws=ws)
+    run_steps(0, 1)
     torch.cuda.synchronize()
     kern = {k: B.timing_read(k) for k in B.KINDS}
     B.timing_enable(False)
     kern[DOMINANT] = dom
 
+    dt = float(np.median(times))
     n_tok = B.num_tokens(n_vals, sp)
-    tok_done = min(n_tok, (args.warmup + args.steps) * Bw * W) - args.warmup * Bw * W
     tok_per_value = n_tok / max(n_vals, 1)
+    tok_step = min(Bw * W, n_tok) if reuse else Bw * W
+    tok_done = tok_step * args.steps
     grad_bytes = tok_done / tok_per_value * w.serial.bytes_per_value
     value = grad_bytes / dt / 1e6
     ms_step = dt * 1e3 / args.steps
 
+    f32 = w.model.dtype == "f32"
+    peak = PEAK_F32_VECTOR_TFLOPS if f32 else PEAK_BF16_TFLOPS
     flops_step = {k: model.flops(Bw, W, k) for k in B.KINDS}
     total_flops = sum(flops_step.values())
-    mfma_util = total_flops * args.steps / dt / (PEAK_BF16_TFLOPS * 1e12)
+    mfma_util = None if f32 else total_flops * args.steps / dt / (PEAK_BF16_TFLOPS * 1e12)
     ms_k, n_k = kern[DOMINANT]
     launches_per_step = w.model.n_layers
     flop_launch = flops_step[DOMINANT] / launches_per_step
     avg_ms = ms_k / max(n_k, 1)
     achieved = flop_launch / (avg_ms * 1e-3) / 1e12
-    traffic = load_traffic(args.traffic_json)
-    kernel_ms = {k: round(ms / (args.steps if k == DOMINANT else 1), 3) for k, (ms, n) in kern.items() if n}
+    traffic = load_traffic(args.traffic_json) if w.name == "7b" and not f32 else None
+    kernel_ms = {k: round(ms / (args.steps * args.repeats if k == DOMINANT else 1), 3)
+                 for k, (ms, n) in kern.items() if n}
+    ms_list = sorted(t * 1e3 / args.steps for t in times)
 
     out = {
         "metric": "gradient MB/s compressed (LM probs + AC) at 7B-shape bf16; MFMA util",
@@ -287,42 +358,52 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded Laplace gradients, random-init weights)",
+        "dtype": "f32" if f32 else "bf16",
+        "data": "synthetic (seeded " + w.dist.split(":")[0] + " gradients, random-init weights)",
         "config": {
             "workload": f"{w.name}: {describe_model(w.model)}, gradients ~ {w.dist}"
                         + (f" then {w.lossy}" if w.lossy else "")
                         + f", {describe_serial(w.serial, tok_per_value)}",
             "windows_per_step": Bw,
             "window_tokens": W,
-            "tokens_per_step": Bw * W,
-            "values_per_step": round(Bw * W / tok_per_value, 1),
+            "tokens_per_step": tok_step,
+            "values_per_step": round(tok_step / tok_per_value, 1),
+            "windows_reused_every_step": reuse,
             "parallelism": "single GPU",
         },
+        "repeats": {"n": args.repeats, "steps_each": args.steps,
+                    "ms_per_step": [round(x, 3) for x in ms_list],
+                    "median_ms": round(ms_step, 3),
+                    "spread_pct": round(100.0 * (ms_list[-1] - ms_list[0]) / ms_step, 2)},
         "tokens_per_s": round(tok_done / dt, 1),
-        "mfma_util": round(mfma_util, 4),
+        "mfma_util": None if mfma_util is None else round(mfma_util, 4),
         "container_bytes": len(buf),
-        "compression_rate_pct": round(100.0 * len(buf) / grad_bytes, 2),
+        "compression_rate_pct": round(100.0 * len(buf) / (tok_step / tok_per_value * w.serial.bytes_per_value
+                                                           * (args.steps if per_call else 1)), 2),
         "kernel_ms_per_step": kernel_ms,
         "roofline": {
-            "kernel": f"{DOMINANT} (gate/up projection {Bw * W}x{2 * w.model.d_ff}x{w.model.d_model} "
-                      "with fused SwiGLU)",
-            "bound": "mfma",
-            "achieved": round(achieved, 1),
-            "peak": PEAK_BF16_TFLOPS,
+            "kernel": f"{DOMINANT} ({'fc' if w.model.arch == 'gpt2' else 'gate/up'} projection "
+                      f"{Bw * W}x{(1 if w.model.arch == 'gpt2' else 2) * w.model.d_ff}x{w.model.d_model} "
+                      f"with fused {'GELU' if w.model.arch == 'gpt2' else 'SwiGLU'}"
+                      + (", float32 FMA kernel" if f32 else "") + ")",
+            "bound": "alu" if f32 else "mfma",
+            "achieved": round(achieved, 2),
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "frac": round(achieved / peak, 4),
             "traffic": traffic,
             "avg_launch_ms": round(avg_ms, 4),
             "flop_per_launch": flop_launch,
         },
     }
+    if w.serial.bytes_per_value != 4:
+        # the lossy stream's values stand for float32 gradients of 4 bytes each
+        out["f32_equivalent_MB_per_s"] = round(tok_done / tok_per_value * 4 / dt / 1e6, 6)
     if lossy_ms is not None:
         out["lossy_prep_ms"] = round(lossy_ms, 3)
-    if not args.no_cpu_baseline and not w.lossy:
+    if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
-        cb = cpu_baseline(w, host, values, args.cpu_sample_values)
-        out["cpu_baseline"] = {k: v for k, v in cb.items() if k != "seconds"}
+        out["cpu_baseline"] = cpu_baseline(w, host, values, args.cpu_positions, args.cpu_positions_one)
     print(json.dumps(out), flush=True)
     model.close()
 

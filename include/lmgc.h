@@ -424,6 +424,31 @@ int lmgc_op_gemm_bf16(const uint16_t* d_a, const uint16_t* d_b, float* d_c, int3
                       int32_t N, int32_t K, void* stream);
 
 /*
+ * The decoder's own matrix-product instantiations (weights in MFMA blocks,
+ * fused epilogues), exposed so that tests check what the model runs at full
+ * size.  B [N, K] bfloat16 in MFMA blocks (lmgc_op_block_weights), A [M, K]
+ * row-major bfloat16, float32 accumulation, K % 64 == 0, N % 256 == 0.
+ *   LMGC_OP_STORE:  out float32 [M, N] = A B^T (the operand ring holds B
+ *                   when N >= 2K, as for the LM head and QKV projections);
+ *   LMGC_OP_RESID:  out float32 [M, N] += A B^T (the residual add of the O
+ *                   and down projections; the ring holds A);
+ *   LMGC_OP_SWIGLU: out bfloat16 [M, N/2]: B's rows are gate and up rows
+ *                   interleaved in groups of 32 (row 64g + t is gate feature
+ *                   32g + t, row 64g + 32 + t its up row, t < 32), and
+ *                   out[m, f] = bf16(silu(gate) * up) (the gate/up
+ *                   projection, the dominant kernel).
+ * Pointers 16-byte aligned, device memory.  GPU, async.  Errors: EINVAL.
+ */
+enum { LMGC_OP_STORE = 0, LMGC_OP_RESID = 1, LMGC_OP_SWIGLU = 2 };
+int lmgc_op_gemm_bf16_blocked(const uint16_t* d_a, const uint16_t* d_b, void* d_out, int32_t M,
+                              int32_t N, int32_t K, int32_t kind, void* stream);
+/* Row-major bfloat16 [N, K] -> MFMA blocks (16 rows x 32 k per 1 KB, lane
+ * order of the 16x16x32 MFMA's B operand): the layout the model keeps its
+ * weights in.  N % 16 == 0, K % 32 == 0, d_dst != d_src.  GPU, async. */
+int lmgc_op_block_weights(const uint16_t* d_src, uint16_t* d_dst, int32_t N, int32_t K,
+                          void* stream);
+
+/*
  * Causal attention kernel of the decoder on bfloat16 operands (the model
  * the paper runs, Sec. 5.1): q [B, Hq, W, hd] and k [B, Hkv, W, hd]
  * row-major, v given TRANSPOSED as vt [B, Hkv, hd, W] (the layout the bf16

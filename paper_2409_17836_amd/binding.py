@@ -101,6 +101,8 @@ def lib():
         "lmgc_decode": (ctypes.c_int, [vp, vp, sz, i32, u64, vp, sz, vp, vp]),
         "lmgc_container_info": (ctypes.c_int, [vp, sz, P(i64), P(i32), P(i64), P(u64)]),
         "lmgc_op_gemm_bf16": (ctypes.c_int, [vp, vp, vp, i32, i32, i32, vp]),
+        "lmgc_op_gemm_bf16_blocked": (ctypes.c_int, [vp, vp, vp, i32, i32, i32, i32, vp]),
+        "lmgc_op_block_weights": (ctypes.c_int, [vp, vp, i32, i32, vp]),
         "lmgc_op_attention_bf16": (ctypes.c_int, [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]),
         "lmgc_timing_enable": (ctypes.c_int, [i32]),
         "lmgc_timing_kinds": (ctypes.c_int, [u32]),
@@ -482,6 +484,33 @@ def op_gemm_bf16(a, b, c=None, stream=None):
         c = torch.empty((M, N), dtype=torch.float32, device=a.device)
     _check(lib().lmgc_op_gemm_bf16(_ptr(a), _ptr(b), _ptr(c), M, N, K, _stream(stream)))
     return c
+
+
+OP_KINDS = {"store": 0, "resid": 1, "swiglu": 2}
+
+
+def op_block_weights(b, stream=None):
+    """b [N, K] bf16 CUDA tensor (row-major) -> the same matrix in MFMA blocks."""
+    import torch
+    N, K = b.shape
+    out = torch.empty_like(b)
+    _check(lib().lmgc_op_block_weights(_ptr(b), _ptr(out), N, K, _stream(stream)))
+    return out
+
+
+def op_gemm_bf16_blocked(a, b_blocked, kind: str, out=None, stream=None):
+    """The model's blocked-weight product with its epilogue: "store" (float32
+    [M, N] = a b^T), "resid" (out += a b^T; out given), "swiglu" (bf16
+    [M, N/2], b's rows gate/up interleaved in groups of 32)."""
+    import torch
+    M, K = a.shape
+    N = b_blocked.shape[0]
+    if out is None:
+        out = (torch.empty((M, N // 2), dtype=torch.bfloat16, device=a.device) if kind == "swiglu"
+               else torch.zeros((M, N), dtype=torch.float32, device=a.device))
+    _check(lib().lmgc_op_gemm_bf16_blocked(_ptr(a), _ptr(b_blocked), _ptr(out), M, N, K, OP_KINDS[kind],
+                                           _stream(stream)))
+    return out
 
 
 def op_attention_bf16(q, k, vt, o=None, stream=None):

@@ -1212,6 +1212,52 @@ int lmgc_op_gemm_bf16(const uint16_t* d_a, const uint16_t* d_b, float* d_c, int3
   return LMGC_OK;
 }
 
+int lmgc_op_block_weights(const uint16_t* d_src, uint16_t* d_dst, int32_t N, int32_t K, void* stream) {
+  clear_error();
+  if (!d_src || !d_dst || N <= 0 || K <= 0) return set_error(LMGC_EINVAL, "bad arguments");
+  if (N % 16 || K % 32) return set_error(LMGC_EINVAL, "need N %% 16 == 0 and K %% 32 == 0");
+  if (((uintptr_t)d_src & 15) || ((uintptr_t)d_dst & 15)) return set_error(LMGC_EINVAL, "pointers must be 16-byte aligned");
+  if (d_src == d_dst) return set_error(LMGC_EINVAL, "d_dst must not be d_src");
+  hipError_t err = launch_gather_rows_blocked(GatherSrcs{{d_src, nullptr, nullptr, nullptr}}, nullptr, N, K, d_dst,
+                                              (hipStream_t)stream);
+  if (err != hipSuccess) return set_error(LMGC_EDEVICE, "block launch: %s", hipGetErrorString(err));
+  return LMGC_OK;
+}
+
+int lmgc_op_gemm_bf16_blocked(const uint16_t* d_a, const uint16_t* d_b, void* d_out, int32_t M, int32_t N,
+                              int32_t K, int32_t kind, void* stream) {
+  clear_error();
+  if (!d_a || !d_b || !d_out || M < 0 || N <= 0 || K <= 0) return set_error(LMGC_EINVAL, "bad arguments");
+  if (K % 64 || N % 256) return set_error(LMGC_EINVAL, "need K %% 64 == 0 and N %% 256 == 0");
+  if (((uintptr_t)d_a & 15) || ((uintptr_t)d_b & 15) || ((uintptr_t)d_out & 15))
+    return set_error(LMGC_EINVAL, "pointers must be 16-byte aligned");
+  EpiArgs e = {};
+  e.M = M;
+  e.N = N;
+  switch (kind) {
+    case LMGC_OP_STORE:
+      e.kind = EPI_STORE_F32;
+      e.c = (float*)d_out;
+      e.ldc = N;
+      break;
+    case LMGC_OP_RESID:
+      e.kind = EPI_RESID;
+      e.c = (float*)d_out;
+      e.ldc = N;
+      break;
+    case LMGC_OP_SWIGLU:
+      e.kind = EPI_SWIGLU;
+      e.out = d_out;
+      e.ld_out = N / 2;
+      break;
+    default:
+      return set_error(LMGC_EINVAL, "unknown kind %d", kind);
+  }
+  hipError_t err = launch_gemm_bf16(d_a, d_b, M, N, K, e, (hipStream_t)stream, true);
+  if (err != hipSuccess) return set_error(LMGC_EDEVICE, "gemm launch: %s", hipGetErrorString(err));
+  return LMGC_OK;
+}
+
 int lmgc_op_attention_bf16(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_vt, uint16_t* d_o,
                            int32_t B, int32_t Hq, int32_t Hkv, int32_t W, int32_t hd, void* stream) {
   clear_error();

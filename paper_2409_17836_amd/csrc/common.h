@@ -164,7 +164,7 @@ struct GatherSrcs {
 hipError_t launch_gather_rows(GatherSrcs srcs, const int32_t* idx, int rows, int cols,
                               int elem_bytes, void* dst, hipStream_t s);
 // The same gather of bf16 rows, written in MFMA blocks (rows % 16 == 0,
-// cols % 32 == 0).
+// cols % 32 == 0); idx == nullptr: row r of srcs.p[0] (no reordering).
 hipError_t launch_gather_rows_blocked(GatherSrcs srcs, const int32_t* idx, int rows, int cols,
                                       void* dst, hipStream_t s);
 

@@ -295,7 +295,7 @@ __global__ void gather_rows_blocked_kernel(GatherSrcs srcs, const int32_t* __res
   if (t >= (int64_t)rows * pieces) return;
   const int r = (int)(t / pieces), q = (int)(t - (int64_t)r * pieces);
   const int64_t di = blocked_index(r, 8 * q, cols) / 8;
-  const int32_t id = idx[r];
+  const int32_t id = idx ? idx[r] : r;
   if (id < 0) {
     dst[di] = make_uint4(0u, 0u, 0u, 0u);
     return;

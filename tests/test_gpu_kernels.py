@@ -91,3 +91,65 @@ def test_attention_full_7b_shape_sampled():
         p = np.exp(s - s.max())
         ref = (p / p.sum()) @ v[b, h, :i + 1].astype(np.float64)
         np.testing.assert_allclose(o[b, i, h], ref, rtol=1e-2, atol=1e-2, err_msg=str((b, h, i)))
+
+
+def _silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+def _blocked_case(kind, M, N, K, seed):
+    """The model's blocked-weight product with its fused epilogue; returns
+    (A, B, C0 or None, output tensor)."""
+    import torch
+    a = bf16_values(gen_normal((M, K), seed))
+    b = bf16_values(gen_normal((N, K), seed + 1))
+    bb = B.op_block_weights(bf16_tensor(b))
+    c0 = None
+    if kind == "resid":
+        c0 = gen_normal((M, N), seed + 2)
+        out = B.op_gemm_bf16_blocked(bf16_tensor(a), bb, "resid", out=torch.from_numpy(c0).cuda())
+    else:
+        out = B.op_gemm_bf16_blocked(bf16_tensor(a), bb, kind)
+    torch.cuda.synchronize()
+    return a, b, c0, out
+
+
+def _blocked_check(kind, a_rows, b, c0_rows, got, K):
+    acc = a_rows.astype(np.float64) @ b.astype(np.float64).T
+    tol = 2e-4 * np.sqrt(K)
+    if kind == "store":
+        np.testing.assert_allclose(got, acc, rtol=1e-5, atol=tol)
+    elif kind == "resid":
+        np.testing.assert_allclose(got, c0_rows.astype(np.float64) + acc, rtol=1e-5, atol=tol)
+    else:
+        # row 64g + t is gate feature 32g + t, row 64g + 32 + t its up row;
+        # the kernel rounds silu(gate) * up to bf16 (one ulp = 2^-8 relative)
+        g = acc.reshape(acc.shape[0], -1, 2, 32)
+        ref = (_silu(g[:, :, 0]) * g[:, :, 1]).reshape(acc.shape[0], -1)
+        np.testing.assert_allclose(got, ref, rtol=2.0 ** -8, atol=1e-3 * np.sqrt(K))
+
+
+@pytest.mark.parametrize("kind", ["store", "resid", "swiglu"])
+@pytest.mark.parametrize("M,N,K", [(300, 512, 128), (1000, 768, 3072), (17, 256, 64)])
+def test_gemm_blocked_small_shapes(kind, M, N, K):
+    """Ragged M (partial row tiles) element by element."""
+    log(f"blocked gemm {kind} {M}x{N}x{K}")
+    a, b, c0, out = _blocked_case(kind, M, N, K, 41)
+    _blocked_check(kind, a, b, c0, out.float().cpu().numpy(), K)
+
+
+@pytest.mark.parametrize("kind,N,K", [("swiglu", 22016, 4096), ("resid", 4096, 11008),
+                                      ("resid", 4096, 4096), ("store", 12288, 4096),
+                                      ("store", 32000, 4096)])
+def test_gemm_blocked_full_7b_shapes_sampled(kind, N, K):
+    """The instantiations the 7B-shape model runs (weights in MFMA blocks;
+    operand ring on B for the wide products, on A for the residual adds) at
+    M = 8 windows x 4096 tokens: 64 sampled rows, every column."""
+    import torch
+    M = 32768
+    log(f"blocked gemm full {kind} {M}x{N}x{K}")
+    a, b, c0, out = _blocked_case(kind, M, N, K, 51)
+    rng = np.random.default_rng(N + K)
+    rows = np.unique(np.concatenate([rng.integers(0, M, 60), [0, 255, 256, M - 1]]))
+    got = out[torch.from_numpy(rows).cuda()].float().cpu().numpy()
+    _blocked_check(kind, a[rows], b, None if c0 is None else c0[rows], got, K)
