@@ -69,27 +69,44 @@ __device__ inline void rope_rot(float vlo, float vhi, float c, float s, float& l
 // it writes the log-sum-exp partial (max m, sum of exp(z - m)) and the
 // logits of the alphabet columns; launch_head_tables merges the partials.
 // In all three matrix kernels (tiled bf16, decoding-step bf16, float32) a
-// group's 64 values of one row sit in 16 lanes of a wave, lane t holding
-// columns t + 16 j, j = 0..3, so one function reduces them for all three
-// and the encoder's and decoder's tables agree bit for bit.
+// group's 64 values of one row sit in one row of 16 lanes (lanes 16 k ..
+// 16 k + 15) of a wave, lane t holding columns t + 16 j, j = 0..3, so one
+// function reduces them for all three and the encoder's and decoder's
+// tables agree bit for bit.
 constexpr float kLog2e = 1.4426950408889634f;
+
+// One DPP exchange within each row of 16 lanes (row_mirror: lane l <-> 15 -
+// l; row_half_mirror: l <-> 7 - l in each half; quad_perm 1,0,3,2 / 2,3,0,1:
+// l <-> l ^ 1 / l ^ 2).  Every lane has a source, so no lane keeps `old`.
+constexpr int kDppRowMirror = 0x140, kDppRowHalfMirror = 0x141, kDppXor1 = 0xB1, kDppXor2 = 0x4E;
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
 
 // z[j]: column t + 16 j of the group (-inf past the vocabulary).  The max
 // over the group, then exp(z - max) summed lane-locally in j order and over
-// the 16 lanes by a butterfly (xor 8, 4, 2, 1); max and + are commutative,
-// so all 16 lanes end with the same bits.  Every lane of the wave must call
-// it (it shuffles).
+// the 16 lanes of the row by four DPP exchanges (partners 15 - l, then 7 - l
+// within each half, then l ^ 1, l ^ 2).  Each exchange pairs lanes whose
+// values are already equal group-wise, and + and max are commutative, so all
+// 16 lanes end with the same bits.  A group of -inf only (columns past the
+// vocabulary) gives (-inf, 0): its reference is taken as 0 so every exp is
+// exp(-inf) = 0.  Every lane of the wave must call it (DPP reads the other
+// lanes).
 __device__ inline float2 group_lse_part(const float z[4]) {
   float m = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+  m = fmaxf(m, dpp_f<kDppRowMirror>(m));
+  m = fmaxf(m, dpp_f<kDppRowHalfMirror>(m));
+  m = fmaxf(m, dpp_f<kDppXor1>(m));
+  m = fmaxf(m, dpp_f<kDppXor2>(m));
+  const float ref = m == -INFINITY ? 0.f : m;
   float s = 0.f;
-  if (m != -INFINITY) {
 #pragma unroll
-    for (int j = 0; j < 4; j++) s += __builtin_amdgcn_exp2f((z[j] - m) * kLog2e);
-  }
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  for (int j = 0; j < 4; j++) s += __builtin_amdgcn_exp2f((z[j] - ref) * kLog2e);
+  s += dpp_f<kDppRowMirror>(s);
+  s += dpp_f<kDppRowHalfMirror>(s);
+  s += dpp_f<kDppXor1>(s);
+  s += dpp_f<kDppXor2>(s);
   return make_float2(m, s);
 }
 
@@ -102,16 +119,27 @@ __device__ inline int alpha_index(const EpiArgs& e, int col) {
   return a;
 }
 
-// One row of the head epilogue: z[j] and aidx[j] for the lane's columns
-// t + 16 j of group g; lane16 = t.  store: the row is in range.
-__device__ inline void head_row(const EpiArgs& e, const float z[4], const int aidx[4], int64_t row,
-                                bool store, int g, int lane16) {
-  const float2 p = group_lse_part(z);
-  if (!store) return;
-  if (e.part && lane16 == 0) e.part[row * e.ngroups + g] = p;
+// Four consecutive rows row0 .. row0 + 3 of the head epilogue: z[r][j] and
+// aidx[j] for the lane's columns t + 16 j of group g; lane16 = t.  Rows at or
+// past M are not stored.  Lanes t < 4 of each 16-lane group store the
+// partial of row row0 + t (all 16 lanes hold it).  any_alpha (the same in
+// every lane of the wave): some lane of the wave has an alphabet column.
+__device__ inline void head_rows4(const EpiArgs& e, const float z[4][4], const int aidx[4],
+                                  bool any_alpha, int64_t row0, int64_t M, int g, int lane16) {
+  float2 p[4];
 #pragma unroll
-  for (int j = 0; j < 4; j++)
-    if (aidx[j] >= 0) e.za[row * e.ld_za + aidx[j]] = z[j];
+  for (int r = 0; r < 4; r++) p[r] = group_lse_part(z[r]);
+  if (e.part) {
+    const float2 v = lane16 == 0 ? p[0] : lane16 == 1 ? p[1] : lane16 == 2 ? p[2] : p[3];
+    if (lane16 < 4 && row0 + lane16 < M) e.part[(row0 + lane16) * e.ngroups + g] = v;
+  }
+  if (any_alpha) {
+#pragma unroll
+    for (int j = 0; j < 4; j++)
+#pragma unroll
+      for (int r = 0; r < 4; r++)
+        if (aidx[j] >= 0 && row0 + r < M) e.za[(row0 + r) * e.ld_za + aidx[j]] = z[r][j];
+  }
 }
 
 // Column info of one (col, col + 32) pair.

@@ -4,35 +4,49 @@
 // Both operands are K-contiguous: activations row-major, weights [out, in]
 // in MFMA blocks (BLKB; common.h: 16 rows x 32 k per 1 KB in the order the
 // lanes take their operand) or row-major (the exposed float32-store product).
-// Tile: 256 x 256 output per 512-thread workgroup: eight 64-wide waves, two
-// per SIMD so that one wave's LDS reads and waits overlap the other's matrix
-// instructions; wave (wm, wn) owns rows wm*128 .. +128 and columns
-// wn*64 .. +64 as 8 x 4 blocks of v_mfma_f32_16x16x32_bf16.
+// Tile: 256 x 256 output per 256-thread workgroup: four 64-wide waves, one
+// per SIMD; wave (wm, wn) owns rows wm*128 .. +128 and columns wn*128 .. +128
+// as 8 x 8 blocks of v_mfma_f32_16x16x32_bf16.  The 256 accumulator
+// registers of a lane live in the AGPR file: the MFMAs are issued as inline
+// assembly with the accumulator as an AGPR operand, which keeps the
+// compiler from shuttling accumulators between the two register files.
+// A 128 x 128 wave tile reads a third fewer LDS bytes per flop than 128 x 64.
 //
-// Operand pipeline.  K advances in stages of 64.  Stages go to LDS with
-// buffer loads straight into LDS (no staging registers): one operand through
-// a ring of three 32 KB buffers, loaded two stages ahead, the other through
-// two, loaded one stage ahead (5 x 32 KB = the whole 160 KB LDS).  The ring
-// holds A by default and B when RB is set: the deeper prefetch goes to the
-// operand whose panels miss L2 more often.  A wide weight matrix (N >= 2K:
-// gate/up, QKV, LM head) has new B panels for every wave of tiles, while an
-// XCD's A panels repeat; for a narrow one (the N = d products that add into
-// the residual) B stays cached and A streams.  A wave's eight loads of a
-// stage are spread through its MFMA stream (one after every four MFMAs, three
-// when the ring holds B) instead of being issued in one burst after the
-// barrier: all workgroups
-// bursting at once queue in L2 and roughly double the load latency.  Each
-// buffer is its own __shared__ array, so the compiler can tell the in-flight
-// loads of one buffer from the reads of another.  The buffer resources are
-// per tile with the tile's valid rows as their size: rows past M read as
-// zero (and only feed outputs that are never stored).
+// Operand pipeline.  K advances in stages of 64 (two 32-wide k-steps).
+// Stages go to LDS with buffer loads straight into LDS (no staging
+// registers): one operand through a ring of three 32 KB buffers, the other
+// through two (5 x 32 KB = the whole 160 KB LDS).  The ring holds A by
+// default and B when RB is set: the longer prefetch goes to the operand
+// whose panels miss L2 more often.  A wide weight matrix (N >= 2K: gate/up,
+// QKV, LM head) has new B panels for every wave of tiles, while an XCD's A
+// panels repeat; for a narrow one (the N = d products that add into the
+// residual) B stays cached and A streams.
+//
+// Schedule of stage s (one wave; every memory operation sits between two
+// MFMAs, in this order):
+//  - k-step 0: 64 MFMAs on fragments already in registers; after every
+//    fourth, one LDS read of k-step 1's fragments; after every eighth, one
+//    load of the ring operand of stage s + 2 (into the ring buffer stage
+//    s - 1 used);
+//  - k-step 1: 32 MFMAs; then the wave waits for its own loads of stage
+//    s + 1 and for its LDS reads, and the workgroup meets at a barrier,
+//    which makes stage s + 1 visible and ends every read of stage s;
+//  - the last 32 MFMAs; the first 16 of them carry the LDS reads of stage
+//    s + 1's first k-step (done before the stage ends) and the loads of the
+//    double-buffered operand of stage s + 2 (into the buffer stage s has
+//    just released).
+// So the matrix cores have work queued on both sides of the barrier, and the
+// loads of one operand have a stage, the other's a stage and a half, to
+// arrive.
 //
 // A row-major 256 x 64 operand tile is stored as rows of eight 16-byte
 // chunks; chunk c of row r sits at slot c ^ ((r >> 1) & 7): the 16 lanes that
 // one ds_read_b128 cycle serves read 16 consecutive rows, and the swizzle
 // gives every (row parity, slot) pair once, i.e. all 64 banks.  A blocked B
 // tile is its 32 blocks copied as they are: lane l reads 16 bytes at 16 l of
-// a block, conflict-free without a swizzle.
+// a block, conflict-free without a swizzle.  The buffer resources are per
+// tile with the tile's valid rows as their size: rows past M read as zero
+// (and only feed outputs that are never stored).
 //
 // Determinism: every output element is the same fixed sequence of MFMA
 // accumulations over k regardless of M, of the tile it sits in, and of the
@@ -55,15 +69,17 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int kThreads = 512;
+constexpr int kThreads = 256;
 // row tiles per group of the tile order: 4 when the ring holds A, 8 when it
 // holds B (measured best at the 7B shape)
 constexpr int kGroupM = 4, kGroupMB = 8;
 constexpr int kXcds = 8;
-// MFMAs between two operand loads of a wave (ring on A / ring on B)
-constexpr int kLoadEvery = 4, kLoadEveryB = 3;
-// s_waitcnt immediates (vmcnt in bits 3:0, expcnt and lgkmcnt left at their maxima)
-constexpr int kVmcnt0 = 0xF70, kVmcnt4 = 0xF74;
+// MFMAs of a stage that follow its barrier
+constexpr int kAfterBarrier = 32;
+// s_waitcnt immediates: vmcnt(n) with expcnt and lgkmcnt at their maxima
+// (vmcnt bits 3:0 and 15:14), and lgkmcnt(0) alone
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0xF70; }
+constexpr int kLgkm0 = 0xC07F;
 
 __device__ inline int slot(int row, int chunk) { return row * 8 + (chunk ^ ((row >> 1) & 7)); }
 
@@ -106,53 +122,50 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave >> 1, wn = wave & 1;
 
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A + (int64_t)m0 * K, min(M - m0, BM) * K * 2);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bw + (int64_t)n0 * K, BN * K * 2);
-  // Load i of wave w fills LDS rows (w*4 + i)*8 .. +8 of a stage; lane l lands
-  // at row +l/8, slot l%8 (the hardware writes lane l at base + 16 l), so it
+  // A stage of one operand is 32 loads of 1 KB; wave w issues q = 8 w + i.
+  // Row-major: load q fills LDS rows 8q .. 8q + 7; lane l lands at row
+  // 8q + l/8, slot l%8 (the hardware writes lane l at base + 16 l), so it
   // fetches the logical chunk the swizzle puts there.  The row is part of the
   // lane offset (for the bounds check), the stage's k offset is scalar.
-  int voff[4];
+  // BLKB: a stage's B tile is 32 blocks of 1 KB (16 row groups x two 32-wide
+  // k chunks); load q copies block q = 16 kc + j (row group j, chunk kc of
+  // the stage) to the same place in LDS, where lane l's 16 bytes are already
+  // its MFMA operand.
+  int voffa[8], voffb[8];
 #pragma unroll
-  for (int i = 0; i < 4; i++) {
-    const int row = (wave * 4 + i) * 8 + (lane >> 3);
+  for (int i = 0; i < 8; i++) {
+    const int q = wave * 8 + i;
+    const int row = q * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ ((row >> 1) & 7);
-    voff[i] = (row * K + lc * 8) * 2;
-  }
-  // BLKB: B in MFMA blocks.  A stage's B tile is 32 blocks of 1 KB (16 row
-  // groups x two 32-wide k chunks); load i of wave w copies block w*4 + i =
-  // 16 kc + j (row group j, chunk kc of the stage) to the same place in LDS,
-  // where lane l's 16 bytes are already its MFMA operand: no swizzle.
-  int voffb[4];
-#pragma unroll
-  for (int i = 0; i < 4; i++) {
-    const int blk = wave * 4 + i, kc = blk >> 4, j = blk & 15;
-    voffb[i] = BLKB ? ((j * (K / 32) + kc) * 1024 + lane * 16) : voff[i];
+    voffa[i] = (row * K + lc * 8) * 2;
+    const int kc = q >> 4, j = q & 15;
+    voffb[i] = BLKB ? ((j * (K / 32) + kc) * 1024 + lane * 16) : voffa[i];
   }
 
-  f32x4 acc[8][4];
+  // zeroed through empty asm statements, so that the zeros are in the AGPRs
+  // before the first (inline) MFMA in program order
+  f32x4 acc[8][8];
 #pragma unroll
   for (int i = 0; i < 8; i++)
 #pragma unroll
-    for (int j = 0; j < 4; j++) acc[i][j] = f32x4{};
+    for (int j = 0; j < 8; j++) asm volatile("" : "=a"(acc[i][j]) : "0"(f32x4{}));
 
   // MFMA operands: lane l supplies row (l & 15) of a 16-row block and the
-  // 8 k-values of chunk (l >> 4) of the 32-wide k step.
-  const int arow0 = wm * 128 + (lane & 15), brow0 = wn * 64 + (lane & 15), kq = lane >> 4;
+  // 8 k-values of chunk (l >> 4) of the 32-wide k-step.
+  const int arow0 = wm * 128 + (lane & 15), brow0 = wn * 128 + (lane & 15), kq = lane >> 4;
 
   auto ldA = [&](u32x4* sa, int i, int k0) __attribute__((always_inline)) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(sa + (wave * 4 + i) * 64), 16, voff[i],
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(sa + (wave * 8 + i) * 64), 16, voffa[i],
                                              k0 * 2, 0, 0);
   };
   auto ldB = [&](u32x4* sb, int i, int k0) __attribute__((always_inline)) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(sb + (wave * 4 + i) * 64), 16, voffb[i],
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr_t)(sb + (wave * 8 + i) * 64), 16, voffb[i],
                                              BLKB ? k0 * 32 : k0 * 2, 0, 0);
   };
-  // One stage from ring buffer sr and double buffer sd.  The double-buffered
-  // operand of stage kd goes to nd and the ring operand of stage kr to nr
-  // (negative: no load), one load after every kLoadEvery (kLoadEveryB) MFMAs.
   auto ld_r = [&](u32x4* buf, int i, int k0) __attribute__((always_inline)) {
     if (RB) ldB(buf, i, k0);
     else ldA(buf, i, k0);
@@ -161,37 +174,23 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     if (RB) ldA(buf, i, k0);
     else ldB(buf, i, k0);
   };
-  auto compute = [&](const u32x4* sr, const u32x4* sd, u32x4* nr, int kr, u32x4* nd, int kd)
+  // Fragments of a k-step: fa/fb for k-step 0 of a stage, ga/gb for k-step 1.
+  // Read r of a k-step: the eight B fragments first (the first eight MFMAs
+  // need all of them), then the A fragments.
+  bf16x8 fa[8], fb[8], ga[8], gb[8];
+  auto rd = [&](bf16x8* xa, bf16x8* xb, const u32x4* sa, const u32x4* sb, int ks, int r)
       __attribute__((always_inline)) {
-    const u32x4* sa = RB ? sd : sr;
-    const u32x4* sb = RB ? sr : sd;
-    int issued = 0, nm = 0;
-#pragma unroll
-    for (int ks = 0; ks < BK / 32; ks++) {
-      const int ch = ks * 4 + kq;
-      bf16x8 af[8], bf[4];
-#pragma unroll
-      for (int i = 0; i < 8; i++) af[i] = as_bf16x8(sa[slot(arow0 + 16 * i, ch)]);
-#pragma unroll
-      for (int j = 0; j < 4; j++)
-        bf[j] = as_bf16x8(BLKB ? sb[(ks * 16 + wn * 4 + j) * 64 + lane] : sb[slot(brow0 + 16 * j, ch)]);
-#pragma unroll
-      for (int i = 0; i < 8; i++)
-#pragma unroll
-        for (int j = 0; j < 4; j++) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
-          if (++nm % (RB ? kLoadEveryB : kLoadEvery) == 0 && issued < 8) {
-            __builtin_amdgcn_sched_barrier(0);
-            if (issued < 4) {
-              if (kd >= 0) ld_d(nd, issued, kd);
-            } else {
-              if (kr >= 0) ld_r(nr, issued - 4, kr);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            issued++;
-          }
-        }
-    }
+    const int ch = ks * 4 + kq;
+    if (r < 8)
+      xb[r] = as_bf16x8(BLKB ? sb[(ks * 16 + wn * 8 + r) * 64 + lane] : sb[slot(brow0 + 16 * r, ch)]);
+    else
+      xa[r - 8] = as_bf16x8(sa[slot(arow0 + 16 * (r - 8), ch)]);
+  };
+  // MFMA n of a k-step: block (n / 8, n % 8)
+  auto mma = [&](const bf16x8* xa, const bf16x8* xb, int n) __attribute__((always_inline)) {
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+                 : "+a"(acc[n >> 3][n & 7])
+                 : "v"(xa[n >> 3]), "v"(xb[n & 7]));
   };
   auto barrier = [&]() __attribute__((always_inline)) {
     __builtin_amdgcn_sched_barrier(0);
@@ -199,109 +198,121 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  // Stage t reads ring buffer t % 3 and double buffer t % 2.  During stage t
-  // a wave loads D(t+1) (into the double buffer stage t-1 used) and R(t+2)
-  // (into the ring buffer of stage t-1), in that order; at the start of stage
-  // t its loads in flight are, oldest first, R(t), D(t), R(t+1), so vmcnt(4)
-  // leaves only R(t+1) outstanding.  The barrier then makes every wave's part
-  // of stage t visible, and ends every wave's reads of stage t-1.
-  auto full = [&](int t, const u32x4* cr, const u32x4* cd, u32x4* nd, u32x4* nr)
-      __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(kVmcnt4);
-    barrier();
-    compute(cr, cd, nr, (t + 2) * BK, nd, (t + 1) * BK);
+  // One stage on buffers (sa, sb); (na, nb) are the next stage's.  NEXT: a
+  // next stage exists (barrier, its first reads); LOADS: stage s + 2 exists
+  // and is loaded (the ring operand into lr, the double-buffered one into
+  // ldb, both at k offset k2).
+  auto stage = [&](auto next_tag, auto loads_tag, const u32x4* sa, const u32x4* sb, const u32x4* na,
+                   const u32x4* nb, u32x4* lr, u32x4* ldb, int k2) __attribute__((always_inline)) {
+    constexpr bool NEXT = decltype(next_tag)::value, LOADS = decltype(loads_tag)::value;
+#pragma unroll
+    for (int n = 0; n < 64; n++) {
+      mma(fa, fb, n);
+      if ((n & 3) == 3) rd(ga, gb, sa, sb, 1, n >> 2);
+      if (LOADS && (n & 7) == 7) ld_r(lr, n >> 3, k2);
+    }
+#pragma unroll
+    for (int n = 0; n < 64 - kAfterBarrier; n++) mma(ga, gb, n);
+    if constexpr (NEXT) {
+      // loads in flight, oldest first: R(s+1), D(s+1), then R(s+2) if
+      // LOADS; stage s + 1 needs the first two
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS ? 8 : 0));
+      __builtin_amdgcn_s_waitcnt(kLgkm0);
+      barrier();
+#pragma unroll
+      for (int n = 64 - kAfterBarrier; n < 64; n++) {
+        const int r = n - (64 - kAfterBarrier);
+        mma(ga, gb, n);
+        if (r < 16) rd(fa, fb, na, nb, 0, r);
+        if (LOADS && r < 16 && (r & 1) == 0) ld_d(ldb, r >> 1, k2);
+      }
+    } else {
+#pragma unroll
+      for (int n = 64 - kAfterBarrier; n < 64; n++) mma(ga, gb, n);
+    }
   };
+  // Stage s reads ring buffer s % 3 and double buffer s % 2; it loads R(s+2)
+  // into ring buffer (s + 2) % 3 and D(s+2) into double buffer s % 2.  The
+  // prologue loads stages 0 and 1.
   const int nk = K / BK;
-  auto tail = [&](int t, const u32x4* cr, const u32x4* cd, u32x4* nd, u32x4* nr)
-      __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(kVmcnt0);
-    barrier();
-    compute(cr, cd, nr, t + 2 < nk ? (t + 2) * BK : -1, nd, t + 1 < nk ? (t + 1) * BK : -1);
-  };
 #pragma unroll
-  for (int i = 0; i < 4; i++) ld_r(sR0, i, 0);
+  for (int i = 0; i < 8; i++) ld_r(sR0, i, 0);
 #pragma unroll
-  for (int i = 0; i < 4; i++) ld_d(sD0, i, 0);
+  for (int i = 0; i < 8; i++) ld_d(sD0, i, 0);
   if (nk > 1) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) ld_r(sR1, i, BK);
+    for (int i = 0; i < 8; i++) ld_r(sR1, i, BK);
+#pragma unroll
+    for (int i = 0; i < 8; i++) ld_d(sD1, i, BK);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(16));
+  } else {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   }
-  // buffers repeat every 6 stages; the loop runs while all six steps and the
-  // loads they issue are in range, the rest (at most 7 stages) is predicated
-  int t = 0;
-  for (; t + 8 <= nk; t += 6) {
-    full(t + 0, sR0, sD0, sD1, sR2);
-    full(t + 1, sR1, sD1, sD0, sR0);
-    full(t + 2, sR2, sD0, sD1, sR1);
-    full(t + 3, sR0, sD1, sD0, sR2);
-    full(t + 4, sR1, sD0, sD1, sR0);
-    full(t + 5, sR2, sD1, sD0, sR1);
+  barrier();
+  // rotating buffer roles: cr/nr/lr the ring buffers of stages s, s + 1 and
+  // s + 2; cd/nd the double buffers of stages s and s + 1
+  u32x4 *cr = sR0, *nr = sR1, *lr = sR2, *cd = sD0, *nd = sD1;
+#define LMGC_A(R, D) (RB ? (D) : (R))
+#define LMGC_B(R, D) (RB ? (R) : (D))
+#pragma unroll
+  for (int r = 0; r < 16; r++) rd(fa, fb, LMGC_A(cr, cd), LMGC_B(cr, cd), 0, r);
+  auto rotate = [&]() __attribute__((always_inline)) {
+    u32x4* t = cr;
+    cr = nr;
+    nr = lr;
+    lr = t;
+    t = cd;
+    cd = nd;
+    nd = t;
+  };
+  int s = 0;
+  for (; s + 2 < nk; s++) {
+    stage(std::true_type{}, std::true_type{}, LMGC_A(cr, cd), LMGC_B(cr, cd), LMGC_A(nr, nd),
+          LMGC_B(nr, nd), lr, cd, (s + 2) * BK);
+    rotate();
   }
-  if (t + 0 < nk) tail(t + 0, sR0, sD0, sD1, sR2);
-  if (t + 1 < nk) tail(t + 1, sR1, sD1, sD0, sR0);
-  if (t + 2 < nk) tail(t + 2, sR2, sD0, sD1, sR1);
-  if (t + 3 < nk) tail(t + 3, sR0, sD1, sD0, sR2);
-  if (t + 4 < nk) tail(t + 4, sR1, sD0, sD1, sR0);
-  if (t + 5 < nk) tail(t + 5, sR2, sD1, sD0, sR1);
-  if (t + 6 < nk) tail(t + 6, sR0, sD0, sD1, sR2);
+  if (s + 1 < nk) {
+    stage(std::true_type{}, std::false_type{}, LMGC_A(cr, cd), LMGC_B(cr, cd), LMGC_A(nr, nd),
+          LMGC_B(nr, nd), lr, cd, 0);
+    rotate();
+  }
+  stage(std::false_type{}, std::false_type{}, LMGC_A(cr, cd), LMGC_B(cr, cd), LMGC_A(nr, nd),
+        LMGC_B(nr, nd), lr, cd, 0);
+#undef LMGC_A
+#undef LMGC_B
+  // The compiler does not know the inline MFMAs write the accumulators, so
+  // it cannot space their first reads: 32 wait states cover the longest
+  // MFMA-write -> VALU-read distance.
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < 8; i++)
+#pragma unroll
+    for (int j = 0; j < 8; j++) asm volatile("" : "+a"(acc[i][j]));
 
-  // Epilogue.  16 x 16 block layout: lane holds column (lane & 15) and rows
-  // 4 (lane >> 4) + r, r = 0..3.  Blocks j and j + 2 give the column pair
-  // (col, col + 32).  Rows 4 (lane >> 4) + 0..3 never straddle a window
-  // (W is a multiple of 8).
+  // Epilogue, one 64-column half of the wave's tile at a time: half h holds
+  // blocks acc[.][4h .. 4h + 3], columns n0 + 128 wn + 64 h + 16 j + (lane &
+  // 15).  16 x 16 block layout: lane holds column (lane & 15) and rows
+  // 4 (lane >> 4) + r, r = 0..3.  Blocks j and j + 2 of a half give the
+  // column pair (col, col + 32).  Rows 4 (lane >> 4) + 0..3 never straddle a
+  // window (W is a multiple of 8).
   // The reads an epilogue needs (residual, RoPE table) for row block i + 1
   // are issued before the stores of block i.  Whole tiles (all but the
   // ragged edges) take a path without row and column checks, so the
   // epilogue stays one basic block.
   using E = Epi<uint16_t, KIND, HD>;
   using Pre4 = typename E::Pre4;
-  const int c0 = n0 + wn * 64 + (lane & 15);
-  if constexpr (KIND == EPI_HEAD) {
-    // the wave's 64 columns are group (n0 + 64 wn) / 64; lane holds columns
-    // c0 + 16 j of rows 4 kq + r of every 16-row block
-    const int g = (n0 + wn * 64) >> 6;
-    bool ok[4];
-    int aidx[4];
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-      ok[j] = c0 + 16 * j < e.N;
-      aidx[j] = ok[j] ? alpha_index(e, c0 + 16 * j) : -1;
-    }
-#pragma unroll
-    for (int i = 0; i < 8; i++)
-#pragma unroll
-      for (int r = 0; r < 4; r++) {
-        const int row = m0 + wm * 128 + 16 * i + 4 * kq + r;
-        float z[4];
-#pragma unroll
-        for (int j = 0; j < 4; j++) z[j] = ok[j] ? acc[i][j][r] : -INFINITY;
-        head_row(e, z, aidx, row, row < M, g, lane & 15);
-      }
-    return;
-  }
-  ColInfo ci0 = E::column(e, c0), ci1 = E::column(e, c0 + 16);
-  if (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS) {
-    // bf16 models have head_dim 64 or 128, so q, k and v and every head are
-    // whole 64-column groups: a wave's columns share segment and head.
-    // Saying so turns the epilogue's q/k/v branches into scalar ones.
-    auto uniform = [](ColInfo& c) __attribute__((always_inline)) {
-      c.valid = __builtin_amdgcn_readfirstlane((int)c.valid) != 0;
-      c.seg = __builtin_amdgcn_readfirstlane(c.seg);
-      c.seg2 = __builtin_amdgcn_readfirstlane(c.seg2);
-      c.head = __builtin_amdgcn_readfirstlane(c.head);
-      c.head2 = __builtin_amdgcn_readfirstlane(c.head2);
-    };
-    uniform(ci0);
-    uniform(ci1);
-  }
   const int W = e.W > 0 ? e.W : 1;
-  // V columns of a whole tile (bf16 QKV): the wave's 128 rows x 64 columns
-  // go through LDS, transposed, so that each V^T row (a dim of a head) is
-  // written as 16-byte pieces of 8 consecutive positions.  A wave's region
-  // is 16 KB: 64 rows (columns) of 128 positions, 16-byte chunks swizzled by
-  // chunk ^ (row & 15).  Needs W % 128 == 0 so the rows lie in one window.
-  auto v_transposed = [&]() __attribute__((always_inline)) {
-    u32x4* reg = (wave < 2 ? sR0 : wave < 4 ? sR1 : wave < 6 ? sR2 : sD0) + (wave & 1) * 1024;
+  constexpr bool kQkv = KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS;
+  // V columns of a whole tile (bf16 QKV): a half's 128 rows x 64 columns go
+  // through LDS, transposed, so that each V^T row (a dim of a head) is
+  // written as 16-byte pieces of 8 consecutive positions.  The region of
+  // (wave, half) is 16 KB of the operand buffers: 64 rows (columns) of 128
+  // positions, 16-byte chunks swizzled by chunk ^ (row & 15).  Needs
+  // W % 128 == 0 so the rows lie in one window.
+  auto v_transposed = [&](auto h_tag, const ColInfo& ci0, const ColInfo& ci1, int cw)
+      __attribute__((always_inline)) {
+    constexpr int H = decltype(h_tag)::value;
+    u32x4* reg = (wave == 0 ? sR0 : wave == 1 ? sR1 : wave == 2 ? sR2 : sD0) + H * 1024;
     char* regb = reinterpret_cast<char*>(reg);
     const float bl0 = KIND == EPI_QKV_BIAS ? ci0.blo : 0.f, bh0 = KIND == EPI_QKV_BIAS ? ci0.bhi : 0.f;
     const float bl1 = KIND == EPI_QKV_BIAS ? ci1.blo : 0.f, bh1 = KIND == EPI_QKV_BIAS ? ci1.bhi : 0.f;
@@ -312,59 +323,111 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
       for (int j = 0; j < 4; j++) {
         const int kap = (lane & 15) + 16 * j, rho = 16 * i + 4 * kq;
         const float bias = j == 0 ? bl0 : j == 1 ? bl1 : j == 2 ? bh0 : bh1;
-        const bf16x4 val = {(__bf16)(acc[i][j][0] + bias), (__bf16)(acc[i][j][1] + bias),
-                            (__bf16)(acc[i][j][2] + bias), (__bf16)(acc[i][j][3] + bias)};
+        const f32x4 a = acc[i][4 * H + j];
+        const bf16x4 val = {(__bf16)(a[0] + bias), (__bf16)(a[1] + bias), (__bf16)(a[2] + bias),
+                            (__bf16)(a[3] + bias)};
         const int off = kap * 256 + (((rho >> 3) ^ (kap & 15)) << 4) + (rho & 7) * 2;
         *reinterpret_cast<bf16x4*>(regb + off) = val;
       }
-    const int H = KIND == EPI_QKV_ROPE ? e.Hkv : e.Hq;
+    const int Hv = KIND == EPI_QKV_ROPE ? e.Hkv : e.Hq;
     const int h = HD ? HD : e.hd;
     const int row0 = m0 + wm * 128, b = row0 / W, pos0 = row0 - b * W;
     // first V column: after q and k (Hq and Hkv heads for RoPE models,
     // Hq and Hq for GPT-2's fused projection)
-    const int vcol0 = n0 + wn * 64 - (KIND == EPI_QKV_ROPE ? e.Hq + e.Hkv : 2 * e.Hq) * h;
+    const int vcol0 = cw - (KIND == EPI_QKV_ROPE ? e.Hq + e.Hkv : 2 * e.Hq) * h;
 #pragma unroll
     for (int t = 0; t < 16; t++) {
       const int c = lane + 64 * t, kap = c >> 4, ch = c & 15;
       const u32x4 val = reg[kap * 16 + (ch ^ (kap & 15))];
       const int cc = vcol0 + kap, head = cc / h, dim = cc - head * h;
-      uint16_t* dst = (uint16_t*)e.v + (((int64_t)b * H + head) * h + dim) * W + pos0 + ch * 8;
+      uint16_t* dst = (uint16_t*)e.v + (((int64_t)b * Hv + head) * h + dim) * W + pos0 + ch * 8;
       *reinterpret_cast<u32x4*>(dst) = val;
+    }
+  };
+  auto half = [&](auto h_tag, auto full_tag) __attribute__((always_inline)) {
+    constexpr int H = decltype(h_tag)::value;
+    constexpr bool FULL = decltype(full_tag)::value;
+    const int cw = n0 + wn * 128 + 64 * H;  // first column of the half
+    const int c0 = cw + (lane & 15);
+    if constexpr (KIND == EPI_HEAD) {
+      // the half's 64 columns are group cw / 64; lane holds columns c0 + 16 j
+      // of rows 4 kq + r of every 16-row block
+      const int g = cw >> 6;
+      bool ok[4];
+      int aidx[4];
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        ok[j] = c0 + 16 * j < e.N;
+        aidx[j] = ok[j] ? alpha_index(e, c0 + 16 * j) : -1;
+      }
+      const bool any_alpha = __any(aidx[0] >= 0 || aidx[1] >= 0 || aidx[2] >= 0 || aidx[3] >= 0);
+#pragma unroll
+      for (int i = 0; i < 8; i++) {
+        float z[4][4];
+#pragma unroll
+        for (int r = 0; r < 4; r++)
+#pragma unroll
+          for (int j = 0; j < 4; j++) z[r][j] = ok[j] ? acc[i][4 * H + j][r] : -INFINITY;
+        head_rows4(e, z, aidx, any_alpha, m0 + wm * 128 + 16 * i + 4 * kq, M, g, lane & 15);
+      }
+    } else {
+      ColInfo ci0 = E::column(e, c0), ci1 = E::column(e, c0 + 16);
+      if constexpr (kQkv) {
+        // bf16 models have head_dim 64 or 128, so q, k and v and every head
+        // are whole 64-column groups: a half's columns share segment and
+        // head.  Saying so turns the epilogue's q/k/v branches into scalar
+        // ones.
+        auto uniform = [](ColInfo& c) __attribute__((always_inline)) {
+          c.valid = __builtin_amdgcn_readfirstlane((int)c.valid) != 0;
+          c.seg = __builtin_amdgcn_readfirstlane(c.seg);
+          c.seg2 = __builtin_amdgcn_readfirstlane(c.seg2);
+          c.head = __builtin_amdgcn_readfirstlane(c.head);
+          c.head2 = __builtin_amdgcn_readfirstlane(c.head2);
+        };
+        uniform(ci0);
+        uniform(ci1);
+        if constexpr (FULL) {
+          if (W % 128 == 0 && ci0.seg == 2) {
+            v_transposed(h_tag, ci0, ci1, cw);
+            return;
+          }
+        }
+      }
+      const int rb = m0 + wm * 128 + 4 * kq;
+      Pre4 q0 = E::template pre4<FULL>(e, ci0, c0, rb, M, rb % W);
+      Pre4 q1 = E::template pre4<FULL>(e, ci1, c0 + 16, rb, M, rb % W);
+#pragma unroll
+      for (int i = 0; i < 8; i++) {
+        const int r0 = rb + 16 * i;
+        const int b = r0 / W, p0 = r0 - b * W;
+        Pre4 n0q = q0, n1q = q1;
+        if (i + 1 < 8) {
+          const int r1 = r0 + 16, p1 = r1 % W;
+          n0q = E::template pre4<FULL>(e, ci0, c0, r1, M, p1);
+          n1q = E::template pre4<FULL>(e, ci1, c0 + 16, r1, M, p1);
+        }
+        const f32x4 x0 = acc[i][4 * H + 0], x1 = acc[i][4 * H + 1];
+        const f32x4 x2 = acc[i][4 * H + 2], x3 = acc[i][4 * H + 3];
+        const float a0[4] = {x0[0], x0[1], x0[2], x0[3]};
+        const float a2[4] = {x2[0], x2[1], x2[2], x2[3]};
+        const float a1[4] = {x1[0], x1[1], x1[2], x1[3]};
+        const float a3[4] = {x3[0], x3[1], x3[2], x3[3]};
+        E::template rows4<FULL>(e, ci0, c0, r0, M, b, p0, a0, a2, q0);
+        E::template rows4<FULL>(e, ci1, c0 + 16, r0, M, b, p0, a1, a3, q1);
+        q0 = n0q;
+        q1 = n1q;
+      }
     }
   };
   auto epilogue = [&](auto full_tag) __attribute__((always_inline)) {
     constexpr bool FULL = decltype(full_tag)::value;
-    if constexpr (FULL && (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS)) {
-      if (W % 128 == 0) {
-        barrier();  // every wave has finished reading the operand buffers
-        if (ci0.seg == 2) {
-          v_transposed();
-          return;
-        }
-      }
+    // the V halves reuse the operand buffers: every wave has finished
+    // reading them
+    if constexpr (FULL && kQkv) {
+      if (W % 128 == 0) barrier();
     }
-    const int rb = m0 + wm * 128 + 4 * kq;
-    Pre4 q0 = E::template pre4<FULL>(e, ci0, c0, rb, M, rb % W);
-    Pre4 q1 = E::template pre4<FULL>(e, ci1, c0 + 16, rb, M, rb % W);
-#pragma unroll
-    for (int i = 0; i < 8; i++) {
-      const int r0 = rb + 16 * i;
-      const int b = r0 / W, p0 = r0 - b * W;
-      Pre4 n0q = q0, n1q = q1;
-      if (i + 1 < 8) {
-        const int r1 = r0 + 16, p1 = r1 % W;
-        n0q = E::template pre4<FULL>(e, ci0, c0, r1, M, p1);
-        n1q = E::template pre4<FULL>(e, ci1, c0 + 16, r1, M, p1);
-      }
-      const float a0[4] = {acc[i][0][0], acc[i][0][1], acc[i][0][2], acc[i][0][3]};
-      const float a2[4] = {acc[i][2][0], acc[i][2][1], acc[i][2][2], acc[i][2][3]};
-      const float a1[4] = {acc[i][1][0], acc[i][1][1], acc[i][1][2], acc[i][1][3]};
-      const float a3[4] = {acc[i][3][0], acc[i][3][1], acc[i][3][2], acc[i][3][3]};
-      E::template rows4<FULL>(e, ci0, c0, r0, M, b, p0, a0, a2, q0);
-      E::template rows4<FULL>(e, ci1, c0 + 16, r0, M, b, p0, a1, a3, q1);
-      q0 = n0q;
-      q1 = n1q;
-    }
+    half(std::integral_constant<int, 0>{}, full_tag);
+    half(std::integral_constant<int, 1>{}, full_tag);
   };
   if (m0 + BM <= M && n0 + BN <= e.N) epilogue(std::true_type{});
   else epilogue(std::false_type{});
@@ -477,14 +540,13 @@ __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t
       ok[j] = col + 16 * j < e.N;
       aidx[j] = ok[j] ? alpha_index(e, col + 16 * j) : -1;
     }
+    const bool any_alpha = __any(aidx[0] >= 0 || aidx[1] >= 0 || aidx[2] >= 0 || aidx[3] >= 0);
+    float z[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int row = 4 * kq + i;
-      float z[4];
+    for (int i = 0; i < 4; i++)
 #pragma unroll
-      for (int j = 0; j < 4; j++) z[j] = ok[j] ? blk[j][i] : -INFINITY;
-      head_row(e, z, aidx, row, row < M, blockIdx.x, r);
-    }
+      for (int j = 0; j < 4; j++) z[i][j] = ok[j] ? blk[j][i] : -INFINITY;
+    head_rows4(e, z, aidx, any_alpha, 4 * kq, M, blockIdx.x, r);
   } else {
     constexpr int NH = NWR / 2;  // the second half of the waves hand over
     if (wave >= NH) part[wave - NH][lane] = acc;

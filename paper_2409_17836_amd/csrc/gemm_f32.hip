@@ -65,14 +65,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
       ok[j] = n0 + tx + 16 * j < e.N;
       aidx[j] = ok[j] ? alpha_index(e, n0 + tx + 16 * j) : -1;
     }
+    const bool any_alpha = __any(aidx[0] >= 0 || aidx[1] >= 0 || aidx[2] >= 0 || aidx[3] >= 0);
+    float z[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int row = m0 + ty * 4 + i;
-      float z[4];
+    for (int i = 0; i < 4; i++)
 #pragma unroll
-      for (int j = 0; j < 4; j++) z[j] = ok[j] ? acc[i][j] : -INFINITY;
-      head_row(e, z, aidx, row, row < M, blockIdx.x, tx);
-    }
+      for (int j = 0; j < 4; j++) z[i][j] = ok[j] ? acc[i][j] : -INFINITY;
+    head_rows4(e, z, aidx, any_alpha, m0 + ty * 4, M, blockIdx.x, tx);
     return;
   }
   // thread columns tx + 16 j: pairs (tx, tx + 32) and (tx + 16, tx + 48)
