@@ -41,15 +41,20 @@ __device__ inline float load_par<float>(const void* p, int i) {
 }
 
 // silu(x) = x / (1 + e^-x) in float32 with the hardware exp2 and reciprocal
-// (about 1 ulp each); the tanh form of GELU.
+// (about 1 ulp each).
 __device__ inline float silu_f(float x) {
   return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * x));
 }
 
+// The tanh form of GELU, 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x +
+// 0.044715 x^3), evaluated as the identical x / (1 + e^(-2u)): one hardware
+// exp2 and one reciprocal instead of a tanh routine (the epilogue runs with
+// one wave per SIMD, where long dependent sequences are not hidden).  e^(-2u)
+// overflows to inf for large negative x, giving x * 0.
 __device__ inline float gelu_tanh_f(float x) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  const float k2 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
   const float inner = __builtin_fmaf(0.044715f * x * x, x, x);  // explicit fusion, as in rope_rot
-  return 0.5f * x * (1.0f + tanhf(k0 * inner));
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(k2 * inner));
 }
 
 // The per-element arithmetic of the residual add and the RoPE rotation, in
