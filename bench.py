@@ -381,6 +381,9 @@ def main():
         "compression_rate_pct": round(100.0 * len(buf) / (tok_step / tok_per_value * w.serial.bytes_per_value
                                                            * (args.steps if per_call else 1)), 2),
         "kernel_ms_per_step": kernel_ms,
+        # GPU-only time of a step: the kernels of lmgc_probs from the events
+        # (the serialiser, about 0.01 ms, is not among the timed kinds)
+        "gpu_ms_per_step": round(sum(kernel_ms.values()), 3),
         "roofline": {
             "kernel": f"{DOMINANT} ({'fc' if w.model.arch == 'gpt2' else 'gate/up'} projection "
                       f"{Bw * W}x{(1 if w.model.arch == 'gpt2' else 2) * w.model.d_ff}x{w.model.d_model} "

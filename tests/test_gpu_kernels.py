@@ -22,7 +22,7 @@ def _gemm_case(M, N, K, seed):
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 256, 64), (513, 512, 128), (1, 256, 4096),
-                                   (1000, 768, 3072), (256, 2304, 768)])
+                                   (1000, 768, 3072), (256, 2304, 768), (257, 256, 320)])
 def test_gemm_small_shapes(M, N, K):
     log(f"gemm {M}x{N}x{K}")
     a, b, c = _gemm_case(M, N, K, 11)
@@ -130,9 +130,12 @@ def _blocked_check(kind, a_rows, b, c0_rows, got, K):
 
 
 @pytest.mark.parametrize("kind", ["store", "resid", "swiglu"])
-@pytest.mark.parametrize("M,N,K", [(300, 512, 128), (1000, 768, 3072), (17, 256, 64)])
+@pytest.mark.parametrize("M,N,K", [(300, 512, 128), (1000, 768, 3072), (17, 256, 64), (300, 512, 192),
+                                   (129, 256, 320), (64, 1024, 448)])
 def test_gemm_blocked_small_shapes(kind, M, N, K):
-    """Ragged M (partial row tiles) element by element."""
+    """Ragged M (partial row tiles) element by element; K from one 64-wide
+    k-stage to several (the stage loop, the stage before the last and the
+    last take different paths)."""
     log(f"blocked gemm {kind} {M}x{N}x{K}")
     a, b, c0, out = _blocked_case(kind, M, N, K, 41)
     _blocked_check(kind, a, b, c0, out.float().cpu().numpy(), K)
