@@ -192,6 +192,7 @@ def decode_bench(B, model, dv, sp, Bw, W, name):
     same = bool(torch.equal(cdf0, cdf1)) and bool(torch.equal(lp0.view(torch.int32), lp1.view(torch.int32)))
     print(json.dumps({"metric": "decoding path, ms per token step (all windows of the batch)",
                       "value": round(dt * 1e3 / W, 4), "unit": "ms", "higher_is_better": False,
+                      "tokens_per_s": round(Bw * W / dt, 1),
                       "workload": name, "windows": Bw, "window_tokens": W, "token_steps": W,
                       "tables_bit_identical_to_encoder": same}), flush=True)
 
@@ -216,6 +217,8 @@ def main():
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_gemm_up_7b.json"))
     ap.add_argument("--decode", action="store_true",
                     help="time the decoding path (per-position tables through the K/V cache) instead")
+    ap.add_argument("--decode-batch", type=int, default=0,
+                    help="windows per decoding step with --decode (default: the workload's batch; at most 32)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run plain copies of this size (counter calibration)")
     args = ap.parse_args()
@@ -275,7 +278,7 @@ def main():
         lossy_ms = (time.perf_counter() - t0) * 1e3
         log(f"[bench] lossy steps {w.lossy}: {lossy_ms:.2f} ms for {w.n_values} values")
     if args.decode:
-        decode_bench(B, model, dv, sp, Bw, W, w.name)
+        decode_bench(B, model, dv, sp, args.decode_batch or Bw, W, w.name)
         return
     n_vals = dv.numel()
     n_win = B.num_windows(n_vals, sp)

@@ -307,8 +307,8 @@ int lmgc_probs(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t 
  * cache.  Each row's arithmetic is the one lmgc_probs does for that row, so
  * d_cdf (and d_logp) equal lmgc_probs' outputs bit for bit; tests use this
  * to check the decoder's path without arithmetic coding.  d_tokens [B, W]
- * device, B <= 16, other arguments and layouts as lmgc_probs.  Workspace:
- * lmgc_step_workspace(m, B, W) bytes (0 if B > 16).  GPU, async.
+ * device, B <= 32, other arguments and layouts as lmgc_probs.  Workspace:
+ * lmgc_step_workspace(m, B, W) bytes (0 if B > 32).  GPU, async.
  */
 size_t lmgc_step_workspace(const lmgc_model* m, int32_t B, int32_t W);
 int lmgc_probs_stepwise(const lmgc_model* m, const int32_t* d_tokens, int32_t B, int32_t W,
@@ -373,7 +373,7 @@ size_t lmgc_container_bound(int64_t n_values, const lmgc_serial_params* p);
 
 /* Device workspace bytes lmgc_compress / lmgc_decode need (the larger of
  * the two: compression holds one batch's activations, decoding the K/V
- * cache of up to min(batch, 16) windows). */
+ * cache of up to min(batch, 32) windows). */
 size_t lmgc_codec_workspace(const lmgc_model* m, int64_t n_values, const lmgc_serial_params* p,
                             int32_t batch);
 
@@ -395,7 +395,7 @@ int lmgc_compress(const lmgc_model* m, const void* d_values, int64_t n_values,
 /*
  * LM-GC decompression (Sec. 4, "Compression": the LM is replayed from BOS
  * and each decoded token is fed back).  Decompress a whole-vector container
- * into values_out (host, n_values * bytes_per_value bytes).  Decodes groups of min(batch, 16) windows token by
+ * into values_out (host, n_values * bytes_per_value bytes).  Decodes groups of min(batch, 32) windows token by
  * token from BOS: each step computes the next position's tables of the
  * group through the K/V cache (as lmgc_probs_stepwise, bit for bit the
  * encoder's tables), the host decodes one symbol per window and its token

@@ -387,7 +387,7 @@ def probs(model: Model, tokens, sp: SerialParams, total: int = 1 << 16, want_log
 def probs_stepwise(model: Model, tokens, sp: SerialParams, total: int = 1 << 16,
                    want_logp: bool = True, ws=None, stream=None):
     """lmgc_probs_stepwise: the same outputs as probs(), computed position by
-    position through the K/V cache (the decoder's path); B <= 16."""
+    position through the K/V cache (the decoder's path); B <= 32."""
     import torch
     B, W = tokens.shape
     assert tokens.dtype == torch.int32 and tokens.is_contiguous()

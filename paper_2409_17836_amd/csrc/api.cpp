@@ -619,7 +619,7 @@ static double probs_flops(const lmgc_model* m, int B, int W, int kind) {
 // One decoding step works on compact rows (one per window) and keeps every
 // layer's K and V of the window group in a cache; q keeps the [B, Hq, W, hd]
 // layout the attention kernel reads (only the current position is written).
-constexpr int kStepMaxB = 16;
+constexpr int kStepMaxB = 32;  // rows of the one-row GEMM kernel
 
 struct StepWs {
   float* h;

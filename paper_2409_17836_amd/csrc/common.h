@@ -107,7 +107,7 @@ hipError_t launch_gemm_bf16(const uint16_t* A, const uint16_t* B, int M, int N_p
                             const EpiArgs& e, hipStream_t s, bool blocked_b = true);
 hipError_t launch_gemm_f32(const float* A, const float* B, int M, int N_pad, int K,
                            const EpiArgs& e, hipStream_t s);
-// Decoding step: M <= 16 rows, each output element accumulated exactly as
+// Decoding step: M <= 32 rows, each output element accumulated exactly as
 // launch_gemm_bf16 accumulates it (same MFMA, operand layout and k order);
 // B in MFMA blocks.
 hipError_t launch_gemm_bf16_rows(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,

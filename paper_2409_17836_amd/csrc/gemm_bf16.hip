@@ -433,16 +433,18 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   else epilogue(std::false_type{});
 }
 
-// Decoding step (M <= 16 rows: one row per window).  Every wave accumulates
-// one 16-column block and runs, for every output element, the same chain as
-// gemm_bf16_kernel: 16x16x32 bf16 MFMAs over the 32-wide k chunks in
-// increasing order, lane l holding row (l & 15) and k values 8*(l >> 4) .. +8
-// of a chunk.  So a row's outputs equal, bit for bit, what the tiled kernel
-// gives that row in a batch of whole windows.  Operands come straight from
-// global memory (the step streams the weights once), kRowsPf chunks ahead.
-// The step is bound by how many weight bytes each wave has in flight, so the
-// waves are spread over as many CUs as the epilogue allows.  NWR waves per
-// workgroup:
+// Decoding step (M <= 32 rows: one row per window).  Every wave accumulates
+// one 16-column block for NRB blocks of 16 rows (NRB = 1 for M <= 16, else
+// 2; both row blocks take the same weight fragment) and runs, for every
+// output element, the same chain as gemm_bf16_kernel: 16x16x32 bf16 MFMAs
+// over the 32-wide k chunks in increasing order, lane l holding row (l & 15)
+// of its row block and k values 8*(l >> 4) .. +8 of a chunk.  So a row's
+// outputs equal, bit for bit, what the tiled kernel gives that row in a batch
+// of whole windows.  Operands come straight from global memory (the step
+// streams the weights once), kRowsPf chunks ahead (fewer with two row
+// blocks, for registers).  The step is bound by how many weight bytes each
+// wave has in flight, so the waves are spread over as many CUs as the
+// epilogue allows.  NWR waves per workgroup:
 //  - 4: 64 columns; waves 2 and 3 hand their accumulators to waves 0 and 1
 //    through LDS, which run the epilogue on the (col, col + 32) pairs (QKV:
 //    the RoPE pairs and the transposed V stores);
@@ -451,14 +453,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
 //  - 1: one block, for the residual add, which pairs nothing (N = d = 4096 has
 //    only 256 blocks: one wave on each CU instead of 64 four-wave groups).
 constexpr int kRowsPf = 16;
+constexpr int kRowsMax = 32;
 
-template <int KIND, int HD, int NWR>
+template <int KIND, int HD, int NWR, int NRB>
 __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t* __restrict__ A,
                                                                   const uint16_t* __restrict__ Bw,
                                                                   int M, int K, EpiArgs e) {
+  constexpr int PF = NRB == 1 ? kRowsPf : 12;  // chunks in flight
   // accumulators handed over: to the pair's first block (QKV: waves 2, 3 to
   // 0, 1), or all to wave 0 (HEAD: waves 1..3, the group's blocks j = 1..3)
-  __shared__ f32x4 part[NWR == 4 ? 3 : 1][64];
+  __shared__ f32x4 part[NWR == 4 ? 3 : 1][NRB][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int c;  // this wave's block
   if (NWR == 4) c = blockIdx.x * 64 + wave * 16;
@@ -466,42 +470,50 @@ __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t
   else c = blockIdx.x * 16;
   const int r = lane & 15, kq = lane >> 4;
   // rows past M re-read row M - 1; they only feed outputs that are not stored
-  const u32x4* pa = reinterpret_cast<const u32x4*>(A + (int64_t)min(r, M - 1) * K + kq * 8);
+  const u32x4* pa[NRB];
+#pragma unroll
+  for (int rb = 0; rb < NRB; rb++)
+    pa[rb] = reinterpret_cast<const u32x4*>(A + (int64_t)min(16 * rb + r, M - 1) * K + kq * 8);
   // B in MFMA blocks: the wave's 16 rows are one contiguous stream of 1 KB
   // blocks, lane l's 16 bytes at 16 l of each
   const int nkc = K / 32;  // A chunk kc starts at u32x4 index 4 * kc
   const u32x4* pb = reinterpret_cast<const u32x4*>(Bw) + (int64_t)(c / 16) * nkc * 64 + lane;
-  f32x4 acc = f32x4{};
-  u32x4 fa[kRowsPf], fb[kRowsPf];
+  f32x4 acc[NRB];
+#pragma unroll
+  for (int rb = 0; rb < NRB; rb++) acc[rb] = f32x4{};
+  u32x4 fa[PF][NRB], fb[PF];
   auto fetch = [&](int u, int kc) __attribute__((always_inline)) {
-    fa[u] = pa[4 * kc];
+#pragma unroll
+    for (int rb = 0; rb < NRB; rb++) fa[u][rb] = pa[rb][4 * kc];
     fb[u] = pb[(int64_t)kc * 64];
   };
   auto mma = [&](int u) __attribute__((always_inline)) {
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[u]), as_bf16x8(fb[u]), acc, 0, 0, 0);
+#pragma unroll
+    for (int rb = 0; rb < NRB; rb++)
+      acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(fa[u][rb]), as_bf16x8(fb[u]), acc[rb], 0, 0, 0);
   };
-  // chunk kc lives in slot kc % kRowsPf.  The steady loop consumes and
-  // refills every slot without conditions (so the loads' wait counts stay
-  // exact); the last chunks drain afterwards.
-  if (nkc >= kRowsPf) {
+  // chunk kc lives in slot kc % PF.  The steady loop consumes and refills
+  // every slot without conditions (so the loads' wait counts stay exact);
+  // the last chunks drain afterwards.
+  if (nkc >= PF) {
 #pragma unroll
-    for (int u = 0; u < kRowsPf; u++) fetch(u, u);
+    for (int u = 0; u < PF; u++) fetch(u, u);
     int kc0 = 0;
-    for (; kc0 + 2 * kRowsPf <= nkc; kc0 += kRowsPf) {
+    for (; kc0 + 2 * PF <= nkc; kc0 += PF) {
 #pragma unroll
-      for (int u = 0; u < kRowsPf; u++) {
+      for (int u = 0; u < PF; u++) {
         mma(u);
-        fetch(u, kc0 + kRowsPf + u);
+        fetch(u, kc0 + PF + u);
       }
     }
-    const int rest = nkc - kc0 - kRowsPf;  // chunks after the loaded ones, < kRowsPf
+    const int rest = nkc - kc0 - PF;  // chunks after the loaded ones, < PF
 #pragma unroll
-    for (int u = 0; u < kRowsPf; u++) {
+    for (int u = 0; u < PF; u++) {
       mma(u);
-      if (u < rest) fetch(u, kc0 + kRowsPf + u);
+      if (u < rest) fetch(u, kc0 + PF + u);
     }
 #pragma unroll
-    for (int u = 0; u < kRowsPf; u++)
+    for (int u = 0; u < PF; u++)
       if (u < rest) mma(u);
   } else {
     for (int kc = 0; kc < nkc; kc++) {
@@ -509,7 +521,7 @@ __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t
       mma(0);
     }
   }
-  // lane holds column c + (lane & 15) and rows 4 kq + i
+  // lane holds column c + (lane & 15) and rows 16 rb + 4 kq + i
   using E = Epi<uint16_t, KIND, HD>;
   const int col = c + r;
   if constexpr (NWR == 1) {
@@ -517,22 +529,22 @@ __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t
     if (col >= e.N) return;
     const float bias = e.bias ? load_par<uint16_t>(e.bias, col) : 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int row = 4 * kq + i;
-      if (row < M) {
-        float* p = e.c + (int64_t)row * e.ldc;
-        p[col] = resid_add(p[col], acc[i], bias);
+    for (int rb = 0; rb < NRB; rb++)
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const int row = 16 * rb + 4 * kq + i;
+        if (row < M) {
+          float* p = e.c + (int64_t)row * e.ldc;
+          p[col] = resid_add(p[col], acc[rb][i], bias);
+        }
       }
-    }
   } else if constexpr (KIND == EPI_HEAD) {
     static_assert(NWR == 4, "the head's groups are 64 columns: four waves");
-    if (wave > 0) part[wave - 1][lane] = acc;
+#pragma unroll
+    for (int rb = 0; rb < NRB; rb++)
+      if (wave > 0) part[wave - 1][rb][lane] = acc[rb];
     __syncthreads();
     if (wave > 0) return;
-    f32x4 blk[4];
-    blk[0] = acc;
-#pragma unroll
-    for (int j = 1; j < 4; j++) blk[j] = part[j - 1][lane];
     bool ok[4];
     int aidx[4];
 #pragma unroll
@@ -541,38 +553,57 @@ __global__ __launch_bounds__(64 * NWR) void gemm_bf16_rows_kernel(const uint16_t
       aidx[j] = ok[j] ? alpha_index(e, col + 16 * j) : -1;
     }
     const bool any_alpha = __any(aidx[0] >= 0 || aidx[1] >= 0 || aidx[2] >= 0 || aidx[3] >= 0);
-    float z[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; i++)
+    for (int rb = 0; rb < NRB; rb++) {
+      f32x4 blk[4];
+      blk[0] = acc[rb];
 #pragma unroll
-      for (int j = 0; j < 4; j++) z[i][j] = ok[j] ? blk[j][i] : -INFINITY;
-    head_rows4(e, z, aidx, any_alpha, 4 * kq, M, blockIdx.x, r);
+      for (int j = 1; j < 4; j++) blk[j] = part[j - 1][rb][lane];
+      float z[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) z[i][j] = ok[j] ? blk[j][i] : -INFINITY;
+      head_rows4(e, z, aidx, any_alpha, 16 * rb + 4 * kq, M, blockIdx.x, r);
+    }
   } else {
     constexpr int NH = NWR / 2;  // the second half of the waves hand over
-    if (wave >= NH) part[wave - NH][lane] = acc;
+#pragma unroll
+    for (int rb = 0; rb < NRB; rb++)
+      if (wave >= NH) part[wave - NH][rb][lane] = acc[rb];
     __syncthreads();
     if (wave >= NH) return;
-    const f32x4 hi = part[wave][lane];  // block c + 32, same lane layout
     const ColInfo ci = E::column(e, col);
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-      const int row = 4 * kq + i;
-      if (row < M) E::row(e, ci, col, row, row, e.dpos, acc[i], hi[i]);
+    for (int rb = 0; rb < NRB; rb++) {
+      const f32x4 hi = part[wave][rb][lane];  // block c + 32, same lane layout
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const int row = 16 * rb + 4 * kq + i;
+        if (row < M) E::row(e, ci, col, row, row, e.dpos, acc[rb][i], hi[i]);
+      }
     }
   }
+}
+
+template <int KIND, int HD, int NRB>
+hipError_t launch_rows_nrb(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
+                           const EpiArgs& e, hipStream_t s) {
+  if constexpr (KIND == EPI_RESID) {
+    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 1, NRB>), dim3(N_pad / 16), dim3(64), 0, s, A, B, M, K, e);
+  } else if constexpr (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS || KIND == EPI_HEAD) {
+    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 4, NRB>), dim3(N_pad / 64), dim3(256), 0, s, A, B, M, K, e);
+  } else {
+    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 2, NRB>), dim3(N_pad / 32), dim3(128), 0, s, A, B, M, K, e);
+  }
+  return hipGetLastError();
 }
 
 template <int KIND, int HD>
 hipError_t launch_rows_one(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
                            const EpiArgs& e, hipStream_t s) {
-  if constexpr (KIND == EPI_RESID) {
-    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 1>), dim3(N_pad / 16), dim3(64), 0, s, A, B, M, K, e);
-  } else if constexpr (KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS || KIND == EPI_HEAD) {
-    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 4>), dim3(N_pad / 64), dim3(256), 0, s, A, B, M, K, e);
-  } else {
-    hipLaunchKernelGGL((gemm_bf16_rows_kernel<KIND, HD, 2>), dim3(N_pad / 32), dim3(128), 0, s, A, B, M, K, e);
-  }
-  return hipGetLastError();
+  return M <= 16 ? launch_rows_nrb<KIND, HD, 1>(A, B, M, N_pad, K, e, s)
+                 : launch_rows_nrb<KIND, HD, 2>(A, B, M, N_pad, K, e, s);
 }
 
 // HD != 0: the QKV kinds of a bf16 model with that head dim; HD == 0: the rest.
@@ -664,7 +695,7 @@ hipError_t launch_kind(const uint16_t* A, const uint16_t* B, int M, int K, int n
 hipError_t launch_gemm_bf16_rows(const uint16_t* A, const uint16_t* B, int M, int N_pad, int K,
                                  const EpiArgs& e, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (M > 16 || !e.step || K % BK != 0 || N_pad % BN != 0) return hipErrorInvalidValue;
+  if (M > kRowsMax || !e.step || K % BK != 0 || N_pad % BN != 0) return hipErrorInvalidValue;
   const bool qkv = e.kind == EPI_QKV_ROPE || e.kind == EPI_QKV_BIAS;
   if (qkv && e.hd == 128) return launch_rows_kind<128>(A, B, M, N_pad, K, e, s);
   if (qkv && e.hd == 64) return launch_rows_kind<64>(A, B, M, N_pad, K, e, s);

@@ -55,6 +55,9 @@ def test_tinyllama_gqa():
     w = get_workload("tinyllama")
     model, _ = build_model(w.model, w.weight_seed, "paper", keep_host=False)
     _compare(w, model, 4, W=320)
+    # 21 windows: the decoding step's one-row kernels take two 16-row blocks,
+    # the second partly filled
+    _compare(w, model, 21, W=64)
     model.close()
 
 
@@ -62,4 +65,14 @@ def test_7b_shape_several_key_tiles():
     w = get_workload("7b")
     model, _ = build_model(w.model, w.weight_seed, "paper", keep_host=False)
     _compare(w, model, 2, W=256)
+    # the largest decoding group: 32 windows, two full 16-row blocks
+    _compare(w, model, 32, W=128)
+    model.close()
+
+
+def test_gpt2_group_of_17():
+    """GELU and the bias epilogues with a second row block of one window."""
+    w = get_workload("gpt2")
+    model, _ = build_model(w.model, w.weight_seed, "perturbed", keep_host=False)
+    _compare(w, model, 17, W=136, values=gen_values(w.dist, 700, 9))
     model.close()

@@ -66,7 +66,7 @@ def test_tiny_two_token_separator_tables(tiny_perturbed):
     import torch
     w, model, om = tiny_perturbed
     ser = dataclasses.replace(w.serial, sep_id=44, sep2_id=32)
-    vals = workload_values(w)[:400]                 # 15 windows (stepwise: B <= 16)
+    vals = workload_values(w)[:400]                 # 15 windows (stepwise: B <= 32)
     sp = B.serial_params(ser)
     nw = B.num_windows(vals.size, sp)
     tok, _ = B.serialize(torch.from_numpy(vals).cuda(), sp, 0, nw)
