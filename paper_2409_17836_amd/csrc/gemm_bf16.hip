@@ -303,6 +303,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
   using Pre4 = typename E::Pre4;
   const int W = e.W > 0 ? e.W : 1;
   constexpr bool kQkv = KIND == EPI_QKV_ROPE || KIND == EPI_QKV_BIAS;
+  constexpr bool kStaged = KIND == EPI_RESID;
   // V columns of a whole tile (bf16 QKV): a half's 128 rows x 64 columns go
   // through LDS, transposed, so that each V^T row (a dim of a head) is
   // written as 16-byte pieces of 8 consecutive positions.  The region of
@@ -342,6 +343,160 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
       const int cc = vcol0 + kap, head = cc / h, dim = cc - head * h;
       uint16_t* dst = (uint16_t*)e.v + (((int64_t)b * Hv + head) * h + dim) * W + pos0 + ch * 8;
       *reinterpret_cast<u32x4*>(dst) = val;
+    }
+  };
+  // q and k columns of a whole tile (bf16 QKV, W % 128 == 0, head dim 64 or
+  // 128): the wave's 128 columns are whole heads of one segment (one head of
+  // 128 dims, or two of 64) and its 128 rows consecutive positions of one
+  // window, so its output is one (hd 128) or two (hd 64) contiguous blocks
+  // of 128 positions x hd in the [B, H, W, hd] layout.  The rotated (or
+  // biased) bf16 values go to the wave's 32 KB of the operand buffers in
+  // that layout, 16-byte chunks of a row swizzled by chunk ^ swz(row), and
+  // are then read back and stored as 16-byte pieces: each store instruction
+  // writes 1 KB of consecutive memory (instead of 4 rows x 32 bytes of
+  // 2-byte pieces).  Values and rounding are those of Epi::rows4.
+  auto qk_staged = [&](int head0, int seg) __attribute__((always_inline)) {
+    constexpr int h = HD == 64 ? 64 : 128;
+    constexpr int RC = h / 8;  // 16-byte chunks per row
+    u32x4* reg = wave == 0 ? sR0 : wave == 1 ? sR1 : wave == 2 ? sR2 : sD0;
+    char* regb = reinterpret_cast<char*>(reg);
+    auto swz = [](int row) __attribute__((always_inline)) { return (2 * (row >> 2)) & (RC - 1); };
+    auto put = [&](int blk, int row, int dim, float v) __attribute__((always_inline)) {
+      const int off = (blk * 128 + row) * (RC * 16) + (((dim >> 3) ^ swz(row)) << 4) + (dim & 7) * 2;
+      *reinterpret_cast<__bf16*>(regb + off) = (__bf16)v;  // round to nearest even
+    };
+    const int cw0 = n0 + wn * 128;
+    const int row0 = m0 + wm * 128, b = row0 / W, pos0 = row0 - b * W;
+    ColInfo ci[2][2];
+#pragma unroll
+    for (int H = 0; H < 2; H++)
+#pragma unroll
+      for (int jp = 0; jp < 2; jp++) ci[H][jp] = E::column(e, cw0 + 64 * H + 16 * jp + (lane & 15));
+    Pre4 q[2][2];
+#pragma unroll
+    for (int H = 0; H < 2; H++)
+#pragma unroll
+      for (int jp = 0; jp < 2; jp++)
+        q[H][jp] = E::template pre4<true>(e, ci[H][jp], cw0 + 64 * H + 16 * jp + (lane & 15),
+                                          row0 + 4 * kq, M, pos0 + 4 * kq);
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+      Pre4 nq[2][2];
+#pragma unroll
+      for (int H = 0; H < 2; H++)
+#pragma unroll
+        for (int jp = 0; jp < 2; jp++) {
+          nq[H][jp] = q[H][jp];
+          if (i + 1 < 8)
+            nq[H][jp] = E::template pre4<true>(e, ci[H][jp], cw0 + 64 * H + 16 * jp + (lane & 15),
+                                               row0 + 16 * (i + 1) + 4 * kq, M,
+                                               pos0 + 16 * (i + 1) + 4 * kq);
+        }
+#pragma unroll
+      for (int H = 0; H < 2; H++)
+#pragma unroll
+        for (int jp = 0; jp < 2; jp++) {
+          const ColInfo& c = ci[H][jp];
+          const f32x4 xl = acc[i][4 * H + jp], xh = acc[i][4 * H + jp + 2];
+#pragma unroll
+          for (int r = 0; r < 4; r++) {
+            const int row = 16 * i + 4 * kq + r;
+            if constexpr (KIND == EPI_QKV_ROPE) {
+              float lo, hi;
+              rope_rot(xl[r], xh[r], q[H][jp].x[r], q[H][jp].y[r], lo, hi);
+              put(c.head - head0, row, c.i, lo);
+              put(c.head - head0, row, c.i + h / 2, hi);
+            } else {
+              put(c.head - head0, row, c.i, xl[r] + c.blo);
+              put(c.head2 - head0, row, c.i2, xh[r] + c.bhi);
+            }
+          }
+        }
+#pragma unroll
+      for (int H = 0; H < 2; H++)
+#pragma unroll
+        for (int jp = 0; jp < 2; jp++) q[H][jp] = nq[H][jp];
+    }
+    const int Hs = KIND == EPI_QKV_ROPE && seg == 1 ? e.Hkv : e.Hq;
+    uint16_t* base = (uint16_t*)(seg == 0 ? e.q : e.k);
+#pragma unroll
+    for (int t = 0; t < 32; t++) {
+      const int c = lane + 64 * t, blk = c / (128 * RC), rem = c - blk * (128 * RC);
+      const int row = rem / RC, ch = rem - row * RC;
+      const u32x4 val = reg[(blk * 128 + row) * RC + (ch ^ swz(row))];
+      uint16_t* dst = base + ((((int64_t)b * Hs + head0 + blk) * W + pos0 + row) * h + ch * 8);
+      *reinterpret_cast<u32x4*>(dst) = val;
+    }
+  };
+  // residual add of a whole tile: the float32 accumulators of one 64-column
+  // half at a time go to the wave's LDS region as [row][64] (16-byte chunks
+  // swizzled by chunk ^ 4 ((row >> 2) & 3)); each lane then reads 4
+  // consecutive columns of a row back and adds them to the residual stream
+  // with 16-byte loads and stores (4 rows x 256 B per instruction), in the
+  // arithmetic of Epi::row_in.  The residual rows are loaded in batches of 8
+  // loads per lane, three batches ahead of the one being added, so the loads
+  // of the second half are in flight while the first half is stored.
+  auto resid_staged = [&]() __attribute__((always_inline)) {
+    u32x4* reg = wave == 0 ? sR0 : wave == 1 ? sR1 : wave == 2 ? sR2 : sD0;
+    float* regf = reinterpret_cast<float*>(reg);
+    auto swz = [](int row) __attribute__((always_inline)) { return (4 * (row >> 2)) & 15; };
+    const int row0 = m0 + wm * 128, ch = lane & 15;
+    // the residual rows through a buffer resource over the wave's 128 rows:
+    // lane offset (row lane / 16, columns 4 ch ..), row 4 t a scalar offset
+    const __amdgpu_buffer_rsrc_t rc =
+        make_rsrc(e.c + (int64_t)row0 * e.ldc + n0 + wn * 128, 128 * e.ldc * 4);
+    const int vo0 = ((lane >> 4) * e.ldc + 4 * ch) * 4;
+    float bs[2][4];
+#pragma unroll
+    for (int H = 0; H < 2; H++)
+#pragma unroll
+      for (int u = 0; u < 4; u++)
+        bs[H][u] = e.bias ? load_par<uint16_t>(e.bias, n0 + wn * 128 + 64 * H + 4 * ch + u) : 0.f;
+    // batch q: half q / 4, loads t = 8 (q % 4) .. + 8 of that half
+    u32x4 x[8][8];
+    auto load_batch = [&](int q) __attribute__((always_inline)) {
+#pragma unroll
+      for (int u = 0; u < 8; u++)
+        x[q][u] = __builtin_amdgcn_raw_buffer_load_b128(rc, vo0 + 256 * (q >> 2),
+                                                        16 * (8 * (q & 3) + u) * e.ldc, 0);
+    };
+    auto to_lds = [&](int H) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < 8; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          const f32x4 a = acc[i][4 * H + j];
+          const int cc = 16 * j + (lane & 15);
+#pragma unroll
+          for (int r = 0; r < 4; r++) {
+            const int row = 16 * i + 4 * kq + r;
+            regf[row * 64 + (((cc >> 2) ^ swz(row)) << 2) + (cc & 3)] = a[r];
+          }
+        }
+    };
+    auto add_batch = [&](int q) __attribute__((always_inline)) {
+      const int H = q >> 2;
+#pragma unroll
+      for (int u = 0; u < 8; u++) {
+        const int t = 8 * (q & 3) + u, row = 4 * t + (lane >> 4);
+        const f32x4 a = reinterpret_cast<const f32x4*>(reg)[row * 16 + (ch ^ swz(row))];
+        const f32x4 xo = __builtin_bit_cast(f32x4, x[q][u]);
+        f32x4 y;
+#pragma unroll
+        for (int k = 0; k < 4; k++) y[k] = resid_add(xo[k], a[k], bs[H][k]);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, y), rc, vo0 + 256 * H,
+                                               16 * t * e.ldc, 0);
+      }
+    };
+    load_batch(0);
+    load_batch(1);
+    load_batch(2);
+    to_lds(0);
+#pragma unroll
+    for (int q = 0; q < 8; q++) {
+      if (q == 4) to_lds(1);  // after the first half's reads, in LDS order
+      add_batch(q);
+      if (q + 3 < 8) load_batch(q + 3);
     }
   };
   auto half = [&](auto h_tag, auto full_tag) __attribute__((always_inline)) {
@@ -423,13 +578,37 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_bf16_kernel(
     constexpr bool FULL = decltype(full_tag)::value;
     // the V halves reuse the operand buffers: every wave has finished
     // reading them
+    if constexpr (FULL && kStaged) {
+      // the LDS regions still hold operands other waves may be reading
+      barrier();
+      resid_staged();
+      return;
+    }
     if constexpr (FULL && kQkv) {
-      if (W % 128 == 0) barrier();
+      if (W % 128 == 0) {
+        barrier();
+        if constexpr (HD == 64 || HD == 128) {
+          // segment and head of the wave's first and last 64 columns
+          const ColInfo c0 = E::column(e, n0 + wn * 128), c1 = E::column(e, n0 + wn * 128 + 64);
+          const int s0 = __builtin_amdgcn_readfirstlane(c0.seg);
+          const int s1 = __builtin_amdgcn_readfirstlane(c1.seg);
+          if (s0 < 2 && s1 == s0) {
+            qk_staged(__builtin_amdgcn_readfirstlane(c0.head), s0);
+            return;
+          }
+        }
+      }
     }
     half(std::integral_constant<int, 0>{}, full_tag);
     half(std::integral_constant<int, 1>{}, full_tag);
   };
-  if (m0 + BM <= M && n0 + BN <= e.N) epilogue(std::true_type{});
+  bool full = m0 + BM <= M && n0 + BN <= e.N;
+  if constexpr (kStaged) {
+    // the staged residual add moves 16-byte pieces of rows; other tiles take
+    // the checked path (kernel arguments: the same for every wave)
+    full = full && (reinterpret_cast<uintptr_t>(e.c) & 15) == 0 && e.ldc % 4 == 0;
+  }
+  if (full) epilogue(std::true_type{});
   else epilogue(std::false_type{});
 }
 
