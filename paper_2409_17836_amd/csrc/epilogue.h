@@ -135,8 +135,14 @@ __device__ inline void head_rows4(const EpiArgs& e, const float z[4][4], const i
 #pragma unroll
   for (int r = 0; r < 4; r++) p[r] = group_lse_part(z[r]);
   if (e.part) {
-    const float2 v = lane16 == 0 ? p[0] : lane16 == 1 ? p[1] : lane16 == 2 ? p[2] : p[3];
-    if (lane16 < 4 && row0 + lane16 < M) e.part[(row0 + lane16) * e.ngroups + g] = v;
+    // selected component by component from scalars: a select between the
+    // float2 elements themselves became a lane-indexed load from a
+    // stack copy of p
+    const float m0 = p[0].x, m1 = p[1].x, m2 = p[2].x, m3 = p[3].x;
+    const float s0 = p[0].y, s1 = p[1].y, s2 = p[2].y, s3 = p[3].y;
+    const float vm = lane16 == 0 ? m0 : lane16 == 1 ? m1 : lane16 == 2 ? m2 : m3;
+    const float vs = lane16 == 0 ? s0 : lane16 == 1 ? s1 : lane16 == 2 ? s2 : s3;
+    if (lane16 < 4 && row0 + lane16 < M) e.part[(row0 + lane16) * e.ngroups + g] = make_float2(vm, vs);
   }
   if (any_alpha) {
 #pragma unroll
