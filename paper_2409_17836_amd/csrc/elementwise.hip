@@ -67,9 +67,10 @@ __global__ void embed_kernel(const int32_t* __restrict__ tokens, int B, int W, i
 // One wave per row; lane l keeps elements l, l+64, ... in registers (general
 // case: any d that is a multiple of 64, float32 or bf16 output).
 template <int MAXV>
-__global__ void norm_kernel(const float* __restrict__ h, int M, int d, const void* __restrict__ g,
-                            const void* __restrict__ b, int layernorm, float eps, int dtype,
-                            void* __restrict__ y) {
+__global__ __launch_bounds__(256) void norm_kernel(const float* __restrict__ h, int M, int d,
+                                                   const void* __restrict__ g,
+                                                   const void* __restrict__ b, int layernorm,
+                                                   float eps, int dtype, void* __restrict__ y) {
   const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (row >= M) return;
