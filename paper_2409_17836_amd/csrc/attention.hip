@@ -72,6 +72,41 @@ __device__ inline uint32_t pack2(float a, float b) {
 
 constexpr float kLazy = 8.0f;  // log2 headroom of the lazily moved softmax reference
 
+// Item k of an XCD's range [r0, r1) of (head, query block) items (item u:
+// head u / nqb, block nqb - 1 - u % nqb, so a head's blocks come longest
+// first).  The long blocks (block >= S) keep that head-major order, which
+// keeps a head's K/V in the XCD's L2 while its blocks run; the short ones
+// (block < S) follow, longest first across the range's heads, so the
+// range ends with short items and no CU waits long on the last ones.
+__device__ inline bool xcd_item(int k, int r0, int r1, int nqb, int S, int& h, int& qb) {
+  if (k >= r1 - r0) return false;
+  const int h0 = r0 / nqb, h1 = (r1 - 1) / nqb;
+  for (int hh = h0; hh <= h1; hh++) {
+    const int ja = hh == h0 ? r0 - hh * nqb : 0;
+    const int jb = hh == h1 ? r1 - hh * nqb : nqb;
+    const int nl = max(0, min(jb, nqb - S) - ja);  // long items of this head
+    if (k < nl) {
+      h = hh;
+      qb = nqb - 1 - (ja + k);
+      return true;
+    }
+    k -= nl;
+  }
+  for (int j = nqb - S; j < nqb; j++)
+    for (int hh = h0; hh <= h1; hh++) {
+      const int ja = hh == h0 ? r0 - hh * nqb : 0;
+      const int jb = hh == h1 ? r1 - hh * nqb : nqb;
+      if (j < ja || j >= jb) continue;
+      if (k == 0) {
+        h = hh;
+        qb = nqb - 1 - j;
+        return true;
+      }
+      k--;
+    }
+  return false;
+}
+
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
@@ -96,13 +131,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
     // Workgroup x of window b runs on XCD x % 8 (gridDim.x is a multiple of
     // 8).  Each XCD gets a contiguous range of the window's (head, query
     // block) items, so all blocks of a head read its K and V through one L2
-    // (spread over the eight L2s, the K/V tiles came from HBM); within a head
-    // the longest blocks go first.
-    const int per = gridDim.x / 8;
-    const int t = ((int)blockIdx.x % 8) * per + (int)blockIdx.x / 8;
-    if (t >= nqb * Hq) return;
-    h = t / nqb;
-    qb = nqb - 1 - (t - h * nqb);
+    // (spread over the eight L2s, the K/V tiles came from HBM); the order
+    // within the range is xcd_item's.
+    const int per = gridDim.x / 8, x = (int)blockIdx.x % 8;
+    const int r0 = x * per, r1 = min(r0 + per, nqb * Hq);
+    if (!xcd_item((int)blockIdx.x / 8, r0, r1, nqb, nqb / 4, h, qb)) return;
   }
   const int kvh = h * Hkv / Hq;
   const int tid = threadIdx.x, lane = tid & 63;
