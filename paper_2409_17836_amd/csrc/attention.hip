@@ -107,7 +107,8 @@ __device__ inline bool xcd_item(int k, int r0, int r1, int nqb, int S, int& h, i
   return false;
 }
 
-template <int HD>
+// DQM: decoding-step mode (only query dq of each window; see below).
+template <int HD, bool DQM>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ vt,
@@ -123,7 +124,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   const int nqb = (W + BQ - 1) / BQ;
   int qb, h;
   const int b = blockIdx.z;
-  if (dq >= 0) {
+  if (DQM) {
     // a decoding step runs only the block of position dq
     qb = dq / BQ;
     h = blockIdx.y;
@@ -141,8 +142,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, c32 = lane & 31;
-  const int q0 = qb * BQ + wave * 32;
+  // A decoding step needs only query dq.  Every wave then takes the 32
+  // queries of dq's wave (the same scores and softmax, bit for bit, in each)
+  // and accumulates one of the NOB 32-dim blocks of P V (wave w: block w, in
+  // oacc[0]; waves past NOB only load), so a tile's critical path is one
+  // wave's S MFMAs and softmax plus a quarter of the P V MFMAs.  Each block's
+  // chain is the one the whole-window pass runs for that query.
+  const int q0 = DQM ? (dq / 32) * 32 : qb * BQ + wave * 32;
   const int myq = q0 + c32;
+  const bool computes = !DQM || wave < NOB;
+  constexpr int NACC = DQM ? 1 : NOB;  // accumulated output blocks
+  // dims of accumulated block i
+  auto oblk = [&](int i) __attribute__((always_inline)) { return DQM ? wave : i; };
 
   const uint16_t* Qp = q + (int64_t)(b * Hq + h) * W * HD;
   const uint16_t* Kp = k + (int64_t)(b * Hkv + kvh) * W * HD;
@@ -155,9 +166,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
     for (int ks = 0; ks < NKS; ks++)
       qf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(Qp + (int64_t)qr * HD + 16 * ks + 8 * half));
   }
-  f32x16 oacc[NOB];
+  f32x16 oacc[NACC];
 #pragma unroll
-  for (int i = 0; i < NOB; i++) oacc[i] = f32x16{};
+  for (int i = 0; i < NACC; i++) oacc[i] = f32x16{};
   float m_i = -INFINITY, l_i = 0.f;
   const float lazy = kLazy / sl2;
 
@@ -281,7 +292,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
         const float alpha = __builtin_amdgcn_exp2f((m_i - mx) * sl2);
         l_i *= alpha;
 #pragma unroll
-        for (int i = 0; i < NOB; i++) oacc[i] *= alpha;
+        for (int i = 0; i < NACC; i++) oacc[i] *= alpha;
         m_i = mx;
       }
     }
@@ -314,14 +325,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
     // k-step outer: the NOB accumulations of a step are independent chains
 #pragma unroll
     for (int kk = 0; kk < 4; kk++) {
-      bf16x8 va[NOB];
+      bf16x8 va[NACC];
 #pragma unroll
-      for (int i = 0; i < NOB; i++) {
-        const int d = i * 32 + c32;
+      for (int i = 0; i < NACC; i++) {
+        const int d = oblk(i) * 32 + c32;
         va[i] = as_bf16x8(sVc[d * 8 + ((2 * kk + half) ^ vswz(d))]);
       }
 #pragma unroll
-      for (int i = 0; i < NOB; i++)
+      for (int i = 0; i < NACC; i++)
         oacc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i], pf[kk], oacc[i], 0, 0, 0);
     }
   };
@@ -340,8 +351,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
     if (t + 2 < ntiles) kload_any(sKf, (t + 2) * BKV);
     if (t + 1 < ntiles) vtload_any(sVf, (t + 1) * BKV);
     __builtin_amdgcn_sched_barrier(0);
-    if (t + 1 <= tlast) qk(sKn, n0, n1);
-    if (t <= tlast) softmax_pv(t, c0, c1, sVc);
+    if (computes && t + 1 <= tlast) qk(sKn, n0, n1);
+    if (computes && t <= tlast) softmax_pv(t, c0, c1, sVc);
     __builtin_amdgcn_sched_barrier(0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   };
@@ -350,7 +361,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   if (ntiles > 1) kload_any(sK1, BKV);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
-  qk(sK0, sa0, sa1);
+  if (computes) qk(sK0, sa0, sa1);
   int t = 0;
   for (; t + 2 <= ntiles; t += 2) {
     step(t, sa0, sa1, sb0, sb1, sK1, sV0, sK0, sV1);
@@ -359,14 +370,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __res
   if (t < ntiles) step(t, sa0, sa1, sb0, sb1, sK1, sV0, sK0, sV1);
 
   l_i += __shfl_xor(l_i, 32, 64);
-  if (dq >= 0 ? myq == dq : myq < W) {
+  if (DQM ? myq == dq && computes : myq < W) {
     const float inv = 1.0f / l_i;
-    uint16_t* orow = o + ((int64_t)b * (dq >= 0 ? 1 : W) + (dq >= 0 ? 0 : myq)) * (int64_t)(Hq * HD) + h * HD;
+    uint16_t* orow = o + ((int64_t)b * (DQM ? 1 : W) + (DQM ? 0 : myq)) * (int64_t)(Hq * HD) + h * HD;
 #pragma unroll
-    for (int i = 0; i < NOB; i++) {
+    for (int i = 0; i < NACC; i++) {
 #pragma unroll
       for (int a = 0; a < 4; a++) {
-        const int d = i * 32 + 8 * a + 4 * half;
+        const int d = oblk(i) * 32 + 8 * a + 4 * half;
         uint2 u;
         u.x = pack2(oacc[i][4 * a + 0] * inv, oacc[i][4 * a + 1] * inv);
         u.y = pack2(oacc[i][4 * a + 2] * inv, oacc[i][4 * a + 3] * inv);
@@ -444,10 +455,14 @@ hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uin
   const int items = (W + 127) / 128 * Hq;  // (head, 128-query block) items per window
   const dim3 grid = dq >= 0 ? dim3(1, Hq, B) : dim3((items + 7) / 8 * 8, 1, B), block(256);
   const float sl2 = (float)(1.4426950408889634 / sqrt((double)hd));
-  if (hd == 128)
-    hipLaunchKernelGGL(attn_bf16_kernel<128>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);
+  if (hd == 128 && dq >= 0)
+    hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);
+  else if (hd == 128)
+    hipLaunchKernelGGL((attn_bf16_kernel<128, false>), grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);
+  else if (hd == 64 && dq >= 0)
+    hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);
   else if (hd == 64)
-    hipLaunchKernelGGL(attn_bf16_kernel<64>, grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);
+    hipLaunchKernelGGL((attn_bf16_kernel<64, false>), grid, block, 0, s, q, k, vt, o, Hq, Hkv, W, sl2, dq);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
