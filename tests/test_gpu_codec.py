@@ -181,3 +181,22 @@ def test_tinyllama_short_roundtrip():
     vals = workload_values(w)[:60]                           # 540 tokens -> 5 windows
     _roundtrip(model, OModel(w.model, host), vals, spec, batch=4)
     model.close()
+
+
+def test_tinyllama_decode_groups_up_to_32():
+    """lmgc_decode with groups of more than 16 windows per step (two 16-row
+    MFMA blocks in the one-row kernels) on a bf16 model: 43 windows of 64
+    tokens, decoded in groups of 32 + 11 and of 20 + 20 + 3, lossless."""
+    import torch
+    w = get_workload("tinyllama")
+    model, _ = build_model(w.model, w.weight_seed, keep_host=False)
+    spec = hex_serial(window=64, bos_id=1)
+    vals = workload_values(w)[:300]                          # 2700 tokens -> 43 windows
+    sp = B.serial_params(spec)
+    assert B.num_windows(vals.size, sp) == 43
+    buf = B.compress(model, torch.from_numpy(vals).cuda(), sp, batch=8, model_tag=9)
+    for batch in (32, 20):
+        log(f"tinyllama decode, batch {batch}")
+        back = B.decode(model, buf, batch=batch, model_tag=9)
+        assert back.tobytes() == vals.tobytes(), f"not lossless with batch {batch}"
+    model.close()
