@@ -76,3 +76,18 @@ def test_gpt2_group_of_17():
     model, _ = build_model(w.model, w.weight_seed, "perturbed", keep_host=False)
     _compare(w, model, 17, W=136, values=gen_values(w.dist, 700, 9))
     model.close()
+
+
+def test_stepwise_group_limit():
+    """At most 32 windows per decoding step: the workspace helper gives 0
+    above that and lmgc_probs_stepwise rejects the call before any GPU work."""
+    import torch
+    w = get_workload("tiny")
+    model, _ = build_model(w.model, 5, "perturbed", keep_host=False)
+    assert model.step_workspace(32, 64) > 0
+    assert model.step_workspace(33, 64) == 0
+    sp = B.serial_params(w.serial)
+    tok = torch.ones((33, 64), dtype=torch.int32, device="cuda")
+    with pytest.raises(B.LMGCError):
+        B.probs_stepwise(model, tok, sp, ws=B.workspace(1 << 20, tok.device))
+    model.close()
