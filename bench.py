@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 matrix peak
 PEAK_F32_VECTOR_TFLOPS = 157.3     # MI355X float32 vector peak (the tiny model's FMA kernels)
+HBM_PEAK_GBS = 8000.0              # MI355X HBM3E bandwidth (the decoding step is bound by it)
 DOMINANT = "gemm_up"               # gate/up projection + SwiGLU: 44% of the FLOPs
 
 
@@ -172,7 +173,20 @@ def copy_calibration(mib):
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "copies": 3}), flush=True)
 
 
-def decode_bench(B, model, dv, sp, Bw, W, name):
+def decode_step_bytes(m, Bw, W, wbytes):
+    """HBM bytes one decoding step must move, averaged over a window of W
+    positions: every weight matrix once (the step's products read each
+    layer's weights whatever the number of windows) and, in attention, the
+    K and V of positions 0..p of every window at position p."""
+    d, hd, F, V = m.d_model, m.head_dim, m.d_ff, m.vocab
+    per_layer = (m.n_heads + 2 * m.n_kv_heads) * hd * d + d * d
+    per_layer += (2 * F * d + F * d) if m.arch == "llama" else (F * d + d * F)
+    weights = (m.n_layers * per_layer + V * d) * wbytes
+    kv_mean = m.n_layers * 2 * m.n_kv_heads * hd * wbytes * Bw * (W + 1) / 2.0
+    return weights + kv_mean
+
+
+def decode_bench(B, model, dv, sp, Bw, W, name, mshape=None):
     """The decoder's path: lmgc_probs_stepwise computes the tables one
     position at a time through the K/V cache, all Bw windows of the batch per
     token step, as lmgc_decode does between its host decoding steps.  Timed
@@ -190,11 +204,19 @@ def decode_bench(B, model, dv, sp, Bw, W, name):
     dt = time.perf_counter() - t0
     cdf0, lp0 = B.probs(model, tok, sp)
     same = bool(torch.equal(cdf0, cdf1)) and bool(torch.equal(lp0.view(torch.int32), lp1.view(torch.int32)))
-    print(json.dumps({"metric": "decoding path, ms per token step (all windows of the batch)",
-                      "value": round(dt * 1e3 / W, 4), "unit": "ms", "higher_is_better": False,
-                      "tokens_per_s": round(Bw * W / dt, 1),
-                      "workload": name, "windows": Bw, "window_tokens": W, "token_steps": W,
-                      "tables_bit_identical_to_encoder": same}), flush=True)
+    line = {"metric": "decoding path, ms per token step (all windows of the batch)",
+            "value": round(dt * 1e3 / W, 4), "unit": "ms", "higher_is_better": False,
+            "tokens_per_s": round(Bw * W / dt, 1),
+            "workload": name, "windows": Bw, "window_tokens": W, "token_steps": W,
+            "tables_bit_identical_to_encoder": same}
+    if mshape is not None:
+        # the step is bound by HBM: weights once per step plus the K/V prefix
+        nb = decode_step_bytes(mshape, Bw, W, 2 if mshape.dtype == "bf16" else 4)
+        ach = nb / (dt / W) / 1e9
+        line["roofline"] = {"bound": "hbm", "algorithmic_GB_per_step": round(nb / 1e9, 3),
+                            "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": round(ach / HBM_PEAK_GBS, 4)}
+    print(json.dumps(line), flush=True)
 
 
 def main():
@@ -278,7 +300,7 @@ def main():
         lossy_ms = (time.perf_counter() - t0) * 1e3
         log(f"[bench] lossy steps {w.lossy}: {lossy_ms:.2f} ms for {w.n_values} values")
     if args.decode:
-        decode_bench(B, model, dv, sp, args.decode_batch or Bw, W, w.name)
+        decode_bench(B, model, dv, sp, args.decode_batch or Bw, W, w.name, w.model)
         return
     n_vals = dv.numel()
     n_win = B.num_windows(n_vals, sp)
